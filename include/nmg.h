@@ -1,0 +1,160 @@
+/*
+ * nmg.h -- C ABI of the grouped n:m (n:m:g) sparse-weight library for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * Paper: STen (arXiv 2304.07613), Section 5 "Grouped n:m Sparsity".
+ *
+ * LAYOUT (Section 5, opening paragraph: the n:m nonzero pattern is repeated
+ * over the g rows of a group).  A dense weight W is M x K, row-major, with
+ * leading dimension ldw >= K (elements).  Along K it is cut into
+ * C = ceil(K / m) chunks of m consecutive columns; the last chunk has width
+ * r = K - (C - 1) * m and must satisfy r >= n.  Rows [G*g, G*g + g) form group
+ * G (M must be a multiple of g).  Inside every chunk all rows of a group keep
+ * the same n columns.
+ *
+ *   values  : M x (C*n) elements of the layout's type, row-major, contiguous.
+ *             values[r*(C*n) + c*n + s] is the s-th kept weight of row r in
+ *             chunk c.
+ *   indices : (M/g) x (C*n) bytes, row-major, contiguous.
+ *             indices[G*(C*n) + c*n + s] is the in-chunk offset o of that
+ *             weight (absolute column c*m + o); the n offsets of a chunk are
+ *             strictly ascending.
+ *
+ * SELECTION (Section 5.2: the converter keeps the n:m:g-valid tensor of
+ * largest L1 norm).  Groups and chunks do not constrain one another, so the
+ * optimum keeps, per (group, chunk), the n columns of largest group score
+ *     score[j] = |W[G*g][c*m+j]| + |W[G*g+1][c*m+j]| + ... + |W[G*g+g-1][c*m+j]|
+ * summed in binary32 in that row order, starting from +0 (binary16 weights
+ * are widened exactly first; no flush of subnormals).  Equal scores go to the
+ * lower offset; a NaN score orders above every number and NaNs tie.
+ *
+ * PRODUCT (Section 5.1, the sparse x dense GEMM): Y = W_s * X, where W_s is
+ * the dense matrix the layout represents, X is K x N (row-major, leading
+ * dimension ldx >= N) and Y is M x N (row-major, leading dimension ldy >= N).
+ * Accumulation is binary32; binary16 outputs are rounded to nearest even.
+ *
+ * CONVENTIONS FOR EVERY CALL
+ *   - All data pointers are device pointers (HIP global memory) of the current
+ *     device.  The caller allocates and owns every buffer; the library keeps
+ *     no pointer after a call returns and allocates no device memory.
+ *   - Work is enqueued on `stream` (0 = the null stream) and runs
+ *     asynchronously; a call returns after validation and launch.  Calls are
+ *     thread-safe: the library has no mutable global state.
+ *   - Arguments are validated on the host before anything is launched; on an
+ *     error nothing is enqueued and no output is written.
+ *   - Floating-point inputs must be finite for the product; the selection is
+ *     defined for every input, NaN included.
+ */
+#ifndef NMG_H
+#define NMG_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum nmg_status {
+    NMG_OK = 0,
+    NMG_ERR_NULL = 1,        /* a required pointer is NULL                     */
+    NMG_ERR_PARAM = 2,       /* n, m, g, a size or a leading dimension invalid */
+    NMG_ERR_SHAPE = 3,       /* M % g != 0, or the tail chunk is narrower than n */
+    NMG_ERR_DTYPE = 4,       /* unknown element type                           */
+    NMG_ERR_ALIGN = 5,       /* a pointer or leading dimension is misaligned   */
+    NMG_ERR_LAUNCH = 6,      /* the HIP runtime reported an error on launch    */
+    NMG_ERR_UNSUPPORTED = 7  /* the requested kernel cannot run this layout    */
+} nmg_status;
+
+typedef enum nmg_dtype {
+    NMG_F32 = 0,             /* IEEE binary32 */
+    NMG_F16 = 1              /* IEEE binary16 (accumulation stays binary32) */
+} nmg_dtype;
+
+/* Shape of one n:m:g weight.  Fill it with nmg_layout_init. */
+typedef struct nmg_layout {
+    int32_t M, K;            /* dense weight is M x K                   */
+    int32_t n, m, g;         /* n kept of every m columns, g rows/group */
+    int32_t C;               /* number of chunks, ceil(K / m)           */
+    nmg_dtype dtype;         /* element type of W, values, X and Y      */
+} nmg_layout;
+
+/* Kernel family for the product (the choice is recorded, not guessed). */
+typedef enum nmg_kernel {
+    NMG_KERNEL_AUTO = 0,     /* the library's choice for this layout        */
+    NMG_KERNEL_VALU = 1,     /* vector-ALU FMA; runs every valid layout      */
+    NMG_KERNEL_MFMA = 2      /* binary32 matrix cores on the gathered g x n
+                                sub-tiles; needs g % 4 == 0 and n dividing
+                                16 with 16*m/n <= 128 (or a smaller power-of-
+                                two window that n divides), else
+                                NMG_ERR_UNSUPPORTED */
+} nmg_kernel;
+
+/* Checks 1 <= n <= m <= 255, g >= 1, M >= 1, K >= 1 (NMG_ERR_PARAM),
+ * M % g == 0 and tail width >= n (NMG_ERR_SHAPE), a known dtype
+ * (NMG_ERR_DTYPE), and fills *layout (C included).  Pure host code. */
+nmg_status nmg_layout_init(nmg_layout *layout, int32_t M, int32_t K, int32_t n,
+                           int32_t m, int32_t g, nmg_dtype dtype);
+
+/* Element count of `values` (M * C * n) and byte count of `indices`
+ * ((M / g) * C * n); -1 for an invalid layout.  Pure host code. */
+int64_t nmg_values_numel(const nmg_layout *layout);
+int64_t nmg_indices_numel(const nmg_layout *layout);
+
+/* Dense -> n:m:g (Section 5.2, the L1-maximising converter, here exact).
+ * W: M x K, leading dimension ldw >= K, element-aligned.  Writes every entry
+ * of values (a bit copy of the kept weights, sign of zero included) and of
+ * indices. */
+nmg_status nmg_compress(const nmg_layout *layout, const void *W, int64_t ldw,
+                        void *values, uint8_t *indices, hipStream_t stream);
+
+/* Y = W_s * X (Section 5.1).  X: K x N, leading dimension ldx; Y: M x N,
+ * leading dimension ldy; N >= 1, ldx >= N, ldy >= N; values, X and Y aligned
+ * to their element size (NMG_ERR_ALIGN).  X rows that start on 16-byte (fp32)
+ * or 8-byte (fp16) boundaries are read with vector loads; other X is read
+ * element by element, more slowly.  `indices` must hold n
+ * strictly ascending in-chunk offsets per (group, chunk), as nmg_compress
+ * writes them; other contents are not detected and give unspecified Y (the
+ * kernels still never read outside X's K rows).  Uses NMG_KERNEL_AUTO. */
+nmg_status nmg_spmm(const nmg_layout *layout, const void *values,
+                    const uint8_t *indices, const void *X, int64_t ldx,
+                    int64_t N, void *Y, int64_t ldy, hipStream_t stream);
+
+/* nmg_spmm with an explicit kernel family. */
+nmg_status nmg_spmm_with(const nmg_layout *layout, nmg_kernel kernel,
+                         const void *values, const uint8_t *indices,
+                         const void *X, int64_t ldx, int64_t N, void *Y,
+                         int64_t ldy, hipStream_t stream);
+
+/* The kernel family NMG_KERNEL_AUTO picks for this layout and N. */
+nmg_kernel nmg_spmm_auto_kernel(const nmg_layout *layout, int64_t N);
+
+/* n:m:g -> dense (end of Section 5.2): W_out (M x K, leading dimension
+ * ldw >= K) gets the kept weights at their columns and +0 elsewhere. */
+nmg_status nmg_densify(const nmg_layout *layout, const void *values,
+                       const uint8_t *indices, void *W_out, int64_t ldw,
+                       hipStream_t stream);
+
+/* Elementwise glue between the layers of a linear stack (not in the paper's
+ * format; BERT's encoder block).  `count` elements, contiguous, same dtype.
+ *   nmg_gelu: out = 0.5 x (1 + erf(x / sqrt 2)), computed in binary32 as
+ *             0.5 x erfc(-x / sqrt 2) (no cancellation for negative x).
+ *   nmg_add : out = a + b, computed in binary32 (exactly rounded for
+ *             binary16 operands).
+ * In-place use (out == in / out == a) is allowed. */
+nmg_status nmg_gelu(nmg_dtype dtype, const void *in, void *out, int64_t count,
+                    hipStream_t stream);
+nmg_status nmg_add(nmg_dtype dtype, const void *a, const void *b, void *out,
+                   int64_t count, hipStream_t stream);
+
+/* Static description of a status code; never NULL. */
+const char *nmg_status_str(nmg_status status);
+
+/* Library version string, e.g. "nmg 0.1.0 gfx950". */
+const char *nmg_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NMG_H */

@@ -1,0 +1,83 @@
+"""The C ABI without a GPU: the library loads, exports every function
+``include/nmg.h`` declares, and validates arguments on the host (no call here
+reaches a kernel launch)."""
+import ctypes
+
+import pytest
+import torch
+
+from paper_2304_07613_amd import build, nmg
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if build.is_stale():
+        build.build()
+    return nmg.lib()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = nmg.header_functions()
+    assert len(names) >= 12
+    for name in names:
+        assert hasattr(lib, name), f"{name} declared in nmg.h but not exported"
+    assert nmg.version().startswith("nmg ")
+
+
+def test_layout_init_validation(lib):
+    L = nmg._Layout()
+    init = lambda *a: lib.nmg_layout_init(ctypes.byref(L), *a)
+    assert init(3072, 768, 1, 4, 8, nmg.F32) == nmg.OK and L.C == 192
+    assert init(768, 3072, 1, 10, 16, nmg.F32) == nmg.OK and L.C == 308
+    assert lib.nmg_values_numel(ctypes.byref(L)) == 768 * 308
+    assert lib.nmg_indices_numel(ctypes.byref(L)) == 48 * 308
+    assert init(768, 768, 2, 4, 4, 7) == nmg.ERR_DTYPE
+    assert init(768, 768, 5, 4, 4, nmg.F32) == nmg.ERR_PARAM      # n > m
+    assert init(768, 768, 0, 4, 4, nmg.F32) == nmg.ERR_PARAM      # n < 1
+    assert init(768, 768, 1, 256, 4, nmg.F32) == nmg.ERR_PARAM    # m > 255
+    assert init(768, 768, 1, 4, 0, nmg.F32) == nmg.ERR_PARAM      # g < 1
+    assert init(0, 768, 1, 4, 1, nmg.F32) == nmg.ERR_PARAM        # M < 1
+    assert init(770, 768, 1, 4, 4, nmg.F32) == nmg.ERR_SHAPE      # M % g
+    assert init(8, 10, 3, 4, 1, nmg.F32) == nmg.ERR_SHAPE         # tail 2 < n
+    assert init(8, 10, 2, 4, 1, nmg.F32) == nmg.OK
+    assert lib.nmg_layout_init(None, 8, 8, 1, 4, 1, nmg.F32) == nmg.ERR_NULL
+
+
+def test_calls_reject_bad_arguments_before_launch(lib):
+    L = nmg._Layout()
+    assert lib.nmg_layout_init(ctypes.byref(L), 64, 64, 1, 4, 8, nmg.F32) == nmg.OK
+    p = ctypes.c_void_p(1 << 20)          # never dereferenced: validation fails first
+    odd = ctypes.c_void_p((1 << 20) + 2)  # not aligned to a binary32 element
+    s = ctypes.c_void_p(0)
+    assert lib.nmg_compress(ctypes.byref(L), None, 64, p, p, s) == nmg.ERR_NULL
+    assert lib.nmg_compress(ctypes.byref(L), p, 63, p, p, s) == nmg.ERR_PARAM
+    assert lib.nmg_spmm(ctypes.byref(L), p, p, p, 32, 33, p, 33, s) == nmg.ERR_PARAM  # ldx < N
+    assert lib.nmg_spmm(ctypes.byref(L), p, p, p, 32, 0, p, 32, s) == nmg.ERR_PARAM   # N = 0
+    assert lib.nmg_spmm(ctypes.byref(L), p, p, odd, 32, 32, p, 32, s) == nmg.ERR_ALIGN
+    assert lib.nmg_spmm(ctypes.byref(L), p, p, p, 32, 32, odd, 32, s) == nmg.ERR_ALIGN
+    assert lib.nmg_spmm(ctypes.byref(L), None, p, p, 32, 32, p, 32, s) == nmg.ERR_NULL
+    assert lib.nmg_densify(ctypes.byref(L), p, p, p, 60, s) == nmg.ERR_PARAM
+    assert lib.nmg_gelu(9, p, p, 10, s) == nmg.ERR_DTYPE
+    assert lib.nmg_add(nmg.F16, p, None, p, 10, s) == nmg.ERR_NULL
+    assert lib.nmg_gelu(nmg.F32, p, p, 0, s) == nmg.OK   # empty input: nothing to launch
+    bad = nmg._Layout(64, 64, 1, 4, 8, 17, nmg.F32)    # inconsistent C
+    assert lib.nmg_compress(ctypes.byref(bad), p, 64, p, p, s) == nmg.ERR_PARAM
+    # g % 4 != 0: the matrix-core kernel declines, the vector kernel is the choice
+    assert lib.nmg_layout_init(ctypes.byref(L), 64, 64, 1, 4, 2, nmg.F32) == nmg.OK
+    assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS["mfma"], p, p, p, 32, 32, p, 32,
+                             s) == nmg.ERR_UNSUPPORTED
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 32) == nmg.KERNELS["valu"]
+    assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 1, 4, 8, nmg.F32) == nmg.OK
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma"]
+
+
+def test_status_strings(lib):
+    for st in range(8):
+        assert nmg.status_str(st)
+    assert nmg.status_str(99) == "unknown status"
+
+
+def test_binding_refuses_cpu_tensors(lib):
+    W = torch.zeros(8, 8)
+    with pytest.raises(ValueError):
+        nmg.compress(W, 1, 4, 4)

@@ -1,0 +1,306 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Bars (written out in each check):
+  - indices, masks, values, densified weights: bit-exact;
+  - binary32 products: |Y - Y_ref| <= 1e-5 * (|W_s| |X|) elementwise;
+  - binary16 in / binary32 accumulate: |Y - Y_ref| <= 2e-2 * (|W_s| |X|);
+  - residual add: bit-exact (binary32 holds the binary16 sum exactly enough
+    for one correct rounding); GELU: within one binary16 ulp.
+Y_ref and |W_s| |X| come from the oracle in binary64 on the same inputs.
+
+Paper: STen (arXiv 2304.07613) Section 5 (layout), 5.1 (product), 5.2
+(converter, conversion back to dense).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2304_07613_amd import build, synth
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+TOL = {torch.float32: 1e-5, torch.float16: 2e-2}
+
+
+@pytest.fixture(scope="module")
+def nmg():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2304_07613_amd import nmg as binding
+    binding.lib()  # raises if the library is not built: no fallback
+    return binding
+
+
+def np_of(t: torch.Tensor) -> np.ndarray:
+    return t.detach().cpu().numpy()
+
+
+def bits(a: np.ndarray) -> np.ndarray:
+    return a.view(np.uint16 if a.dtype == np.float16 else np.uint32)
+
+
+def check_compress(nmg, W, n, m, g, tag=""):
+    """GPU compress == oracle compress, bit for bit; returns both packings."""
+    print(f"[compress] {tag} W{tuple(W.shape)} {W.dtype} {n}:{m}:{g}", flush=True)
+    v, idx, L = nmg.compress(W.to(DEV), n, m, g)
+    torch.cuda.synchronize()
+    rv, ridx = oracle.compress(np_of(W), n, m, g)
+    gv, gidx = np_of(v), np_of(idx)
+    assert np.array_equal(gidx, ridx), f"indices differ at {np.argwhere(gidx != ridx)[:5]}"
+    assert np.array_equal(bits(gv), bits(rv)), "values differ"
+    return v, idx, L, rv, ridx
+
+
+def check_product(Y, Yref, B, dtype, what=""):
+    Yg = np_of(Y).astype(np.float64)
+    err = np.abs(Yg - Yref)
+    bound = TOL[dtype] * B
+    bad = err > bound
+    if bad.any():
+        i = np.argwhere(bad)[0]
+        raise AssertionError(f"{what}: {bad.sum()} outputs out of bound; first {tuple(i)}: "
+                             f"gpu {Yg[tuple(i)]!r} ref {Yref[tuple(i)]!r} bound {bound[tuple(i)]!r}")
+    nz = B > 0
+    return float((err[nz] / B[nz]).max()) if nz.any() else 0.0
+
+
+def spmm_full(nmg, v, idx, L, X, rv, ridx, kernel, tag=""):
+    print(f"[spmm] {tag} {L} N={X.shape[1]} kernel={kernel}", flush=True)
+    Y = nmg.spmm(v, idx, X.to(DEV), L, kernel)
+    torch.cuda.synchronize()
+    Yref, B = oracle.spmm(rv, ridx, np_of(X), L.K, L.n, L.m, L.g)
+    return check_product(Y, Yref, B, L.dtype, f"{tag} {kernel}")
+
+
+def kernels_for(nmg, L, N):
+    ks = ["auto", "valu"]
+    if nmg.lib().nmg_spmm_auto_kernel(__import__("ctypes").byref(L.c), N) == nmg.KERNELS["mfma"]:
+        ks.append("mfma")
+    return ks
+
+
+# ------------------------------------------------------ small, multi-tile
+
+SMALL = [
+    # M,   K,   N,   n, m,   g,   dtype
+    (256, 64, 64, 2, 4, 4, torch.float32),      # exactly one workgroup tile
+    (264, 70, 200, 2, 4, 8, torch.float32),     # ragged rows, K tail 2, ragged N
+    (520, 100, 130, 1, 10, 8, torch.float32),   # 1:10 windows, M % 256 != 0
+    (384, 96, 1000, 1, 4, 32, torch.float32),   # g = 32, many token tiles
+    (128, 96, 77, 2, 8, 16, torch.float16),     # binary16, ragged N
+    (64, 68, 65, 1, 20, 4, torch.float32),      # 1:20, tail chunk of 8
+    (96, 64, 33, 3, 5, 3, torch.float32),       # n = 3, g = 3: vector kernel only
+    (48, 40, 9, 4, 4, 1, torch.float32),        # dense control, g = 1
+    (32, 33, 5, 1, 1, 2, torch.float32),        # m = 1: every column kept
+    (8, 255, 3, 7, 255, 8, torch.float32),      # m = 255, one chunk
+    (4, 4, 1, 1, 4, 4, torch.float32),          # one group, one chunk, N = 1
+    (768, 64, 40, 2, 4, 768, torch.float32),    # g = M
+    (96, 48, 300, 2, 4, 12, torch.float16),     # g = 12 (unit of 4 rows)
+    (512, 128, 260, 4, 8, 8, torch.float32),    # n = 4
+]
+
+
+@pytest.mark.parametrize("M,K,N,n,m,g,dtype", SMALL,
+                         ids=[f"{c[0]}x{c[1]}x{c[2]}-{c[3]}:{c[4]}:{c[5]}-{str(c[6])[6:]}"
+                              for c in SMALL])
+def test_small_shapes(nmg, M, K, N, n, m, g, dtype):
+    W = synth.normal((M, K), 11 + M + K, 0.02, dtype)
+    X = synth.normal((K, N), 12 + N, 1.0, dtype)
+    v, idx, L, rv, ridx = check_compress(nmg, W, n, m, g, "small")
+    dense = nmg.densify(v, idx, L)
+    rd, _ = oracle.densify(rv, ridx, K, n, m, g)
+    assert np.array_equal(bits(np_of(dense)), bits(rd))
+    for kernel in kernels_for(nmg, L, N):
+        spmm_full(nmg, v, idx, L, X, rv, ridx, kernel, "small")
+
+
+# ----------------------------------------------------------- edge cases
+
+def test_ties_signed_zeros_and_nan(nmg):
+    rng = np.random.default_rng(1)
+    W = (rng.integers(-4, 5, size=(64, 96)) / 4.0).astype(np.float32)  # many ties
+    W[0, :8] = -0.0
+    W[3, 10] = np.nan
+    W[9, 20] = np.inf
+    W[17, 30:34] = np.nan
+    Wt = torch.from_numpy(W)
+    for n, m, g in [(2, 4, 4), (1, 4, 8), (2, 8, 16), (3, 8, 1), (1, 10, 2)]:
+        check_compress(nmg, Wt, n, m, g, "ties/nan")
+    v, idx, L, rv, ridx = check_compress(nmg, Wt, 2, 4, 4, "signed zeros")
+    assert np.signbit(np_of(v)[0, :4]).all()
+
+
+def test_subnormal_scores(nmg):
+    rng = np.random.default_rng(2)
+    W = (rng.standard_normal((64, 64)) * 1e-39).astype(np.float32)  # binary32 subnormals
+    check_compress(nmg, torch.from_numpy(W), 1, 4, 8, "f32 subnormal")
+    H = (rng.standard_normal((64, 64)) * 1e-6).astype(np.float16)   # binary16 subnormals
+    check_compress(nmg, torch.from_numpy(H), 2, 8, 4, "f16 subnormal")
+
+
+def test_all_zero_weight(nmg):
+    W = torch.zeros(32, 40)
+    v, idx, L, rv, ridx = check_compress(nmg, W, 2, 8, 8, "zeros")
+    assert (np_of(idx).reshape(-1, 2) == [0, 1]).all()
+    X = synth.normal((40, 70), 5)
+    for kernel in kernels_for(nmg, L, 70):
+        Y = nmg.spmm(v, idx, X.to(DEV), L, kernel)
+        assert (np_of(Y) == 0).all()
+
+
+def test_strided_inputs_and_outputs(nmg):
+    """Leading dimensions larger than the row length (views of wider tensors)."""
+    Wb = synth.normal((128, 100), 21, 0.02)
+    Xb = synth.normal((96, 140), 22)
+    W, X = Wb[:, :96], Xb[:, :128]
+    v, idx, L, rv, ridx = check_compress(nmg, W, 1, 4, 8, "strided W")
+    Ybig = torch.full((128, 136), 7.0, device=DEV)
+    Y = Ybig[:, :128]
+    nmg.spmm_into(L, v, idx, X.to(DEV), Y)
+    torch.cuda.synchronize()
+    Yref, B = oracle.spmm(rv, ridx, np.ascontiguousarray(np_of(X)), 96, 1, 4, 8)
+    check_product(Y, Yref, B, torch.float32, "strided")
+    assert (np_of(Ybig)[:, 128:] == 7.0).all()  # nothing written outside Y
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.float16])
+def test_unaligned_x_rows(nmg, dtype):
+    """X starting one element past a 16-byte boundary, with an odd leading
+    dimension: the element-wise load path."""
+    Wt = synth.normal((64, 40), 3, 0.02, dtype)
+    Xb = synth.normal((40 * 37 + 1,), 4, 1.0, dtype)
+    X = Xb[1:].view(40, 37)
+    v, idx, L, rv, ridx = check_compress(nmg, Wt, 1, 4, 8, "unaligned X")
+    Xd = Xb.to(DEV)[1:].view(40, 37)
+    for kernel in kernels_for(nmg, L, 37):
+        Y = nmg.spmm(v, idx, Xd, L, kernel)
+        torch.cuda.synchronize()
+        Yref, B = oracle.spmm(rv, ridx, np.ascontiguousarray(np_of(X)), 40, 1, 4, 8)
+        check_product(Y, Yref, B, dtype, f"unaligned {kernel}")
+
+
+def test_element_misaligned_pointer_is_rejected(nmg):
+    import ctypes
+    W = synth.normal((32, 32), 3, 0.02).to(DEV)
+    v, idx, L = nmg.compress(W, 1, 4, 8)
+    X = torch.zeros(32, 32, device=DEV)
+    Y = torch.empty(32, 32, device=DEV)
+    st = nmg.lib().nmg_spmm(ctypes.byref(L.c), ctypes.c_void_p(v.data_ptr()),
+                            ctypes.c_void_p(idx.data_ptr()), ctypes.c_void_p(X.data_ptr() + 2),
+                            32, 32, ctypes.c_void_p(Y.data_ptr()), 32, ctypes.c_void_p(0))
+    assert st == nmg.ERR_ALIGN
+
+
+def test_repeatable(nmg):
+    W = synth.normal((512, 768), 31, 0.02).to(DEV)
+    X = synth.normal((768, 512), 32).to(DEV)
+    v, idx, L = nmg.compress(W, 1, 4, 8)
+    Y1 = nmg.spmm(v, idx, X, L)
+    Y2 = nmg.spmm(v, idx, X, L)
+    assert torch.equal(Y1, Y2)
+
+
+# ------------------------------------------------------ the five workloads
+
+def sample_points(M, N, count, seed):
+    rng = np.random.default_rng(seed)
+    rows = np.concatenate([rng.integers(0, M, count), [0, M - 1, M - 1]])
+    cols = np.concatenate([rng.integers(0, N, count), [0, N - 1, 0]])
+    return rows, cols
+
+
+def check_sampled(nmg, v, idx, L, X, Y, rv, ridx, count=4096, seed=0, what=""):
+    rows, cols = sample_points(L.M, X.shape[1], count, seed)
+    Yref, B = oracle.spmm_points(rv, ridx, np_of(X), L.K, L.n, L.m, L.g, rows, cols)
+    Ys = Y[torch.as_tensor(rows, device=Y.device), torch.as_tensor(cols, device=Y.device)]
+    return check_product(Ys, Yref, B, L.dtype, what)
+
+
+@pytest.mark.parametrize("workload", [1, 2, 3])
+def test_workload_single_layer(nmg, workload):
+    wl = synth.WORKLOADS[workload]
+    lin = wl.layers[0]
+    W, X = synth.layer_inputs(workload, 0, lin)
+    v, idx, L, rv, ridx = check_compress(nmg, W, lin.n, lin.m, lin.g, wl.key)
+    dense = nmg.densify(v, idx, L)
+    rd, _ = oracle.densify(rv, ridx, lin.K, lin.n, lin.m, lin.g)
+    assert np.array_equal(bits(np_of(dense)), bits(rd))
+    worst = spmm_full(nmg, v, idx, L, X, rv, ridx, "auto", wl.key)
+    print(f"[{wl.key}] worst |Y-Yref|/B = {worst:.3e}", flush=True)
+
+
+def test_workload_sweep(nmg):
+    wl = synth.WORKLOADS[5]
+    for j, lin in enumerate(wl.layers):
+        W, X = synth.layer_inputs(5, j, lin)
+        v, idx, L, rv, ridx = check_compress(nmg, W, lin.n, lin.m, lin.g, lin.name)
+        Xd = X.to(DEV)
+        for kernel in kernels_for(nmg, L, lin.N):
+            print(f"[spmm] sweep {lin.name} kernel={kernel}", flush=True)
+            Y = nmg.spmm(v, idx, Xd, L, kernel)
+            torch.cuda.synchronize()
+            check_sampled(nmg, v, idx, L, X, Y, rv, ridx, 2048, j, f"{lin.name} {kernel}")
+
+
+def test_workload_bert_stack(nmg):
+    """12 layers of the fp16 linear stack, chained on the GPU; every product,
+    GELU and residual sum is checked against the oracle on the GPU's own input
+    to that step."""
+    from paper_2304_07613_amd.stack import LinearStack
+    layers = synth.WORKLOADS[4].layers
+    stack = LinearStack.from_workload(4, nmg, n=2, m=8, g=8)
+    x = synth.normal((synth.BERT_HIDDEN, synth.BERT_TOKENS), synth.seed_for(4, 0, "X"), 1.0,
+                     torch.float16).to(DEV)
+    for li, layer in enumerate(stack.layers):
+        trace = {}
+        x_next = stack.forward_layer(layer, x, trace)
+        torch.cuda.synchronize()
+        # packed weights equal the oracle's packing of the same dense weight
+        for lin in layers:
+            W = layer.dense[lin.name]
+            rv, ridx = oracle.compress(np_of(W), lin.n, lin.m, lin.g)
+            v, idx, _ = layer.packed[lin.name]
+            assert np.array_equal(np_of(idx), ridx) and np.array_equal(bits(np_of(v)), bits(rv))
+        for name, (inp, out) in trace["linear"].items():
+            v, idx, L = layer.packed[name]
+            rv, ridx = np_of(v), np_of(idx)
+            print(f"[stack] layer {li} {name}", flush=True)
+            check_sampled(nmg, v, idx, L, inp.cpu(), out, rv, ridx, 2048, li, f"L{li} {name}")
+        u, gl = trace["gelu"]
+        ref = oracle.gelu_f16(np_of(u))
+        diff = np.abs(np_of(gl).astype(np.float64) - ref.astype(np.float64))
+        with np.errstate(over="ignore"):
+            ulp = np.spacing(np.abs(ref)).astype(np.float64)
+        assert (diff <= ulp).all(), f"gelu layer {li}"
+        for a, b, s in trace["add"]:
+            assert np.array_equal(bits(np_of(s)), bits(oracle.add_f16(np_of(a), np_of(b)))), \
+                f"residual layer {li}"
+        x = x_next
+    assert torch.isfinite(x.float()).all()
+    assert 0.1 < float(x.float().std()) < 100.0
+
+
+def test_elementwise_glue(nmg):
+    bits16 = torch.arange(65536, dtype=torch.int32).to(torch.int16).view(torch.float16)
+    h = bits16[torch.isfinite(bits16)].contiguous()
+    g = nmg.gelu(h.to(DEV))
+    ref = oracle.gelu_f16(np_of(h))
+    got = np_of(g)
+    hx = np_of(h)
+    with np.errstate(over="ignore"):
+        ulp = np.spacing(np.abs(ref)).astype(np.float64)
+    diff = np.abs(got.astype(np.float64) - ref.astype(np.float64))
+    bad = np.isfinite(ref) & ~(diff <= ulp)
+    assert not bad.any(), (f"{bad.sum()} GELU outputs beyond one binary16 ulp, e.g. "
+                           f"x={hx[bad][:4]} gpu={got[bad][:4]} ref={ref[bad][:4]}")
+    a = synth.normal((1 << 16,), 41, 30.0, torch.float16)
+    b = synth.normal((1 << 16,), 42, 0.01, torch.float16)
+    s = nmg.add(a.to(DEV), b.to(DEV))
+    assert np.array_equal(bits(np_of(s)), bits(oracle.add_f16(np_of(a), np_of(b))))
+    x32 = synth.normal((4099,), 43, 3.0)
+    g32 = np_of(nmg.gelu(x32.to(DEV))).astype(np.float64)
+    from scipy.special import erf
+    xd = np_of(x32).astype(np.float64)
+    assert np.allclose(g32, 0.5 * xd * (1 + erf(xd / np.sqrt(2))), rtol=1e-6, atol=1e-7)
