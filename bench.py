@@ -2,7 +2,7 @@
 
 One step = the whole path on one batch: nmg_compress of a dense weight
 (group score, top-n select, pack) followed by nmg_spmm of the packed weight
-with a 4096-token activation.  Workload: BERT-base FFN up-projection,
+with a 4096-token activation.  Default workload: BERT-base FFN up-projection,
 W 3072 x 768 fp32 ~ N(0, 0.02^2), 1:4 (75% sparse), g = 8, X 768 x 4096 fp32
 ~ N(0, 1); synthetic, seeded.
 
@@ -10,14 +10,21 @@ Inputs are resident in HBM before timing starts.  Steps rotate over enough
 distinct buffer sets (> 1 GB in total) that the 256 MB Infinity Cache cannot
 serve a step from the previous visit.
 
-Prints ONE JSON line (rank 0).  `value` = useful GFLOP (2 N nnz of the sparse
+Default output: ONE JSON line.  `value` = useful GFLOP (2 N nnz of the sparse
 weight) per step / step time; `roofline` describes nmg_spmm, the dominant
 kernel, from HIP events around each of its launches in the timed region;
 `cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
+
+Other modes (not the headline): --workload 1|3 (the other single layers),
+--sweep (the n:m x g sweep, one line per point), --stack (the 12-layer fp16
+BERT-base linear stack), --copy-calibration (a plain device copy of known
+size, for scaling the HBM byte counters).
 """
 from __future__ import annotations
 
 import argparse
+import ctypes
+import hashlib
 import json
 import os
 import re
@@ -41,16 +48,21 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--kernel", choices=("auto", "mfma", "valu"), default="auto")
+    ap.add_argument("--workload", type=int, choices=(1, 2, 3), default=2)
+    ap.add_argument("--sweep", action="store_true")
+    ap.add_argument("--stack", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--rotate-mb", type=float, default=1100.0,
                     help="total size of the rotated buffer sets")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time budget of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-family", action="store_true",
+                    help="skip timing the other kernel family")
     return ap.parse_args()
 
 
 def source_digest() -> str:
-    import hashlib
     with open(os.path.join(ROOT, "paper_2304_07613_amd", "csrc", "nmg.hip"), "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
@@ -72,159 +84,152 @@ def stored_traffic(digest: str):
         return None
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
-              f"(the path shards by tokens with no communication, see DESIGN.md)",
-              file=sys.stderr)
-        sys.exit(2)
+class Ctx:
+    def __init__(self):
+        import torch
 
-    import torch
+        from paper_2304_07613_amd import nmg, synth
+        assert torch.cuda.is_available(), "bench.py needs a GPU"
+        nmg.lib()  # raises if the HIP library is missing: there is no fallback
+        self.torch, self.nmg, self.synth = torch, nmg, synth
+        self.dev = torch.device("cuda:0")
+        self.stream = torch.cuda.current_stream(self.dev)
+        self.sp = ctypes.c_void_p(self.stream.cuda_stream)
 
-    from paper_2304_07613_amd import nmg, synth
+    def event(self):
+        return self.torch.cuda.Event(enable_timing=True)
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    nmg.lib()  # raises if the HIP library is missing: there is no fallback
-    dev = torch.device("cuda:0")
-    wl = synth.FFN_UP
-    lin = wl.layers[0]
+
+def layer_bytes(lin, L):
+    es = lin.dtype.itemsize
+    packed = L.M * L.C * L.n * es + (L.M // L.g) * L.C * L.n
+    return {
+        "spmm": packed + lin.K * lin.N * es + lin.M * lin.N * es,
+        "compress": lin.M * lin.K * es + packed,
+        "set": lin.M * lin.K * es + packed + lin.K * lin.N * es + lin.M * lin.N * es,
+    }
+
+
+def time_layer(ctx, args, workload, layer_no, lin, kernel_req):
+    """Rotated resident buffers, warmup, then K timed steps of compress + spmm
+    with HIP events around every launch.  Returns timings and the buffers."""
+    torch, nmg = ctx.torch, ctx.nmg
     L = nmg.Layout(lin.M, lin.K, lin.n, lin.m, lin.g, lin.dtype)
-    kernel = nmg.auto_kernel(L, lin.N) if args.kernel == "auto" else args.kernel
-
-    # ---- resident, rotated inputs and outputs
-    es = 4
-    set_bytes = (lin.M * lin.K + lin.K * lin.N + lin.M * lin.N + L.M * L.C * L.n) * es + \
-        (L.M // L.g) * L.C * L.n
-    n_sets = max(2, int(args.rotate_mb * 1e6 // set_bytes) + 1)
+    kernel = nmg.auto_kernel(L, lin.N) if kernel_req == "auto" else kernel_req
+    nb = layer_bytes(lin, L)
+    n_sets = max(2, int(args.rotate_mb * 1e6 // nb["set"]) + 1)
     sets = []
     for i in range(n_sets):
-        W, X = synth.layer_inputs(2, i, lin)
-        W, X = W.to(dev), X.to(dev)
-        v = torch.empty(L.values_shape, dtype=lin.dtype, device=dev)
-        idx = torch.empty(L.indices_shape, dtype=torch.uint8, device=dev)
-        Y = torch.empty((lin.M, lin.N), dtype=lin.dtype, device=dev)
+        W, X = ctx.synth.layer_inputs(workload, layer_no + 100 * i, lin)
+        W, X = W.to(ctx.dev), X.to(ctx.dev)
+        v = torch.empty(L.values_shape, dtype=lin.dtype, device=ctx.dev)
+        idx = torch.empty(L.indices_shape, dtype=torch.uint8, device=ctx.dev)
+        Y = torch.empty((lin.M, lin.N), dtype=lin.dtype, device=ctx.dev)
         sets.append((W, X, v, idx, Y))
-    torch.cuda.synchronize()
-
-    def step(i):
-        W, X, v, idx, Y = sets[i % n_sets]
-        nmg.compress_into(L, W, v, idx)
-        nmg.spmm_into(L, v, idx, X, Y, kernel)
-
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-
-    # ---- timed region: K steps, events around every launch.  The ctypes
-    # arguments are marshalled beforehand so the host never starves the GPU.
-    import ctypes
-    stream = torch.cuda.current_stream(dev)
     lib = nmg.lib()
-    sp = ctypes.c_void_p(stream.cuda_stream)
     lref = ctypes.byref(L.c)
     vp = lambda t: ctypes.c_void_p(t.data_ptr())
-    calls = [((lref, vp(W), lin.K, vp(v), vp(idx), sp),
-              (lref, nmg.KERNELS[kernel], vp(v), vp(idx), vp(X), lin.N, lin.N, vp(Y), lin.N, sp))
-             for (W, X, v, idx, Y) in sets]
+    # arguments marshalled beforehand so the host never starves the GPU
+    calls = [((lref, vp(W), lin.K, vp(v), vp(idx), ctx.sp),
+              (lref, nmg.KERNELS[kernel], vp(v), vp(idx), vp(X), lin.N, lin.N, vp(Y), lin.N,
+               ctx.sp)) for (W, X, v, idx, Y) in sets]
     compress_c, spmm_c = lib.nmg_compress, lib.nmg_spmm_with
-    K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
     status = []
+    for s in range(args.warmup):
+        ca, sa = calls[s % n_sets]
+        status += [compress_c(*ca), spmm_c(*sa)]
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [[ctx.event() for _ in range(3)] for _ in range(K)]
+    start, stop = ctx.event(), ctx.event()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
-    start.record(stream)
+    start.record(ctx.stream)
     for s in range(K):
         ca, sa = calls[s % n_sets]
-        ev[s][0].record(stream)
+        ev[s][0].record(ctx.stream)
         status.append(compress_c(*ca))
-        ev[s][1].record(stream)
+        ev[s][1].record(ctx.stream)
         status.append(spmm_c(*sa))
-        ev[s][2].record(stream)
-    stop.record(stream)
+        ev[s][2].record(ctx.stream)
+    stop.record(ctx.stream)
     torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
     if any(status):
         raise nmg.NmgError(next(x for x in status if x), "timed step")
-    wall = time.perf_counter() - t0
-    ms_step = start.elapsed_time(stop) / K
-    compress_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / K
-    spmm_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / K
+    res = {
+        "L": L, "kernel": kernel, "n_sets": n_sets, "sets": sets, "wall": wall,
+        "ms_step": start.elapsed_time(stop) / K,
+        "compress_ms": sum(e[0].elapsed_time(e[1]) for e in ev) / K,
+        "spmm_ms": sum(e[1].elapsed_time(e[2]) for e in ev) / K,
+        "bytes": nb,
+    }
+    if not args.no_family:
+        res["family"] = family_times(ctx, L, sets, kernel)
+    return res
 
-    useful_flop = lin.useful_flop
-    value = useful_flop / (ms_step * 1e-3) / 1e9
-    alg_bytes = (L.M * L.C * L.n) * es + (L.M // L.g) * L.C * L.n + lin.K * lin.N * es + \
-        lin.M * lin.N * es
-    spmm_tflops = useful_flop / (spmm_ms * 1e-3) / 1e12
-    peak = FP32_MFMA_PEAK_TFLOPS if kernel == "mfma" else FP32_VALU_PEAK_TFLOPS
-    digest = source_digest()
-    traffic = stored_traffic(digest)
-    compress_bytes = lin.M * lin.K * es + (L.M * L.C * L.n) * es + (L.M // L.g) * L.C * L.n
 
-    # ---- kernel-family evidence (outside the timed region)
-    family = {}
-    W0, X0, v0, idx0, Y0 = sets[0]
-    nmg.compress_into(L, W0, v0, idx0)
+def family_times(ctx, L, sets, kernel, reps=20):
+    """Mean spmm time of each kernel family on the same rotated sets (outside
+    the timed region): the evidence behind the automatic choice."""
+    torch, nmg = ctx.torch, ctx.nmg
+    out = {}
     for fam in ("mfma", "valu"):
         try:
-            for _ in range(3):
-                nmg.spmm_into(L, v0, idx0, X0, Y0, fam)
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            reps = 20
-            e0.record(stream)
+            for r in range(3):
+                W, X, v, idx, Y = sets[r % len(sets)]
+                nmg.spmm_into(L, v, idx, X, Y, fam)
+            e0, e1 = ctx.event(), ctx.event()
+            e0.record(ctx.stream)
             for r in range(reps):
-                Wr, Xr, vr, idxr, Yr = sets[r % n_sets]
-                nmg.spmm_into(L, vr, idxr, Xr, Yr, fam)
-            e1.record(stream)
+                W, X, v, idx, Y = sets[r % len(sets)]
+                nmg.spmm_into(L, v, idx, X, Y, fam)
+            e1.record(ctx.stream)
             torch.cuda.synchronize()
-            family[fam] = round(e0.elapsed_time(e1) / reps * 1e3, 2)
+            out[fam] = round(e0.elapsed_time(e1) / reps * 1e3, 2)
         except nmg.NmgError:
-            family[fam] = None
-    nmg.spmm_into(L, v0, idx0, X0, Y0, kernel)  # set 0 holds the timed kernel's output again
+            out[fam] = None
+    for r in range(len(sets)):  # every set holds the chosen kernel's output again
+        W, X, v, idx, Y = sets[r]
+        nmg.spmm_into(L, v, idx, X, Y, kernel)
     torch.cuda.synchronize()
+    return out
 
-    out = {
-        "metric": METRIC,
-        "value": round(value, 1),
-        "unit": "GFLOP/s",
-        "n_gpus": 1,
-        "steps": K,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic",
-        "config": {"workload": wl.key, "M": lin.M, "K": lin.K, "N": lin.N, "n": lin.n,
-                   "m": lin.m, "g": lin.g, "kernel": kernel, "rotated_sets": n_sets,
-                   "step": "nmg_compress + nmg_spmm"},
+
+def layer_record(lin, res):
+    kernel = res["kernel"]
+    spmm_s = res["spmm_ms"] * 1e-3
+    tflops = lin.useful_flop / spmm_s / 1e12
+    if kernel == "mfma":
+        peak = FP32_MFMA_PEAK_TFLOPS  # binary32 matrix cores for both input types
+    else:
+        peak = FP32_VALU_PEAK_TFLOPS
+    rec = {
         "roofline": {
             "kernel": f"k_spmm_{kernel}",
             "bound": "mfma" if kernel == "mfma" else "alu",
-            "achieved": round(spmm_tflops, 2),
+            "achieved": round(tflops, 2),
             "peak": peak,
             "unit": "TFLOP/s",
-            "frac": round(spmm_tflops / peak, 4),
-            "traffic": traffic,
-            "algorithmic_bytes": alg_bytes,
-            "hbm_frac": round(alg_bytes / (spmm_ms * 1e-3) / (HBM_PEAK_GBS * 1e9), 4),
+            "frac": round(tflops / peak, 4),
+            "traffic": None,
+            "algorithmic_bytes": res["bytes"]["spmm"],
+            "hbm_frac": round(res["bytes"]["spmm"] / spmm_s / (HBM_PEAK_GBS * 1e9), 4),
         },
-        "spmm_us": round(spmm_ms * 1e3, 2),
-        "spmm_gflops": round(useful_flop / (spmm_ms * 1e-3) / 1e9, 1),
-        "compress_us": round(compress_ms * 1e3, 2),
-        "compress_gbs": round(compress_bytes / (compress_ms * 1e-3) / 1e9, 1),
-        "compress_hbm_frac": round(compress_bytes / (compress_ms * 1e-3) / (HBM_PEAK_GBS * 1e9), 4),
-        "spmm_us_by_kernel": family,
-        "wall_s_timed": round(wall, 4),
+        "spmm_us": round(res["spmm_ms"] * 1e3, 2),
+        "spmm_gflops": round(lin.useful_flop / spmm_s / 1e9, 1),
+        "compress_us": round(res["compress_ms"] * 1e3, 2),
+        "compress_gbs": round(res["bytes"]["compress"] / (res["compress_ms"] * 1e-3) / 1e9, 1),
+        "compress_hbm_frac": round(res["bytes"]["compress"] / (res["compress_ms"] * 1e-3) /
+                                   (HBM_PEAK_GBS * 1e9), 4),
     }
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args, lin, L, sets[0], dev)
-    print(json.dumps(out))
+    if "family" in res:
+        rec["spmm_us_by_kernel"] = res["family"]
+    return rec
 
 
-def cpu_baseline(args, lin, L, set0, dev):
+def cpu_baseline(args, lin, L, set0):
     """The CPU oracle (test infrastructure, untuned) on a bounded sample of the
     same workload, on this host's cores; also spot-checks the GPU output of
     that sample against it."""
@@ -239,30 +244,150 @@ def cpu_baseline(args, lin, L, set0, dev):
     rv, ridx = oracle.compress(Wn, lin.n, lin.m, lin.g)
     t_compress = time.perf_counter() - t0
     # calibrate: rows of the product that fit the time budget
-    probe = lin.g * 8
+    probe = lin.g * max(1, 64 // lin.g)
     t0 = time.perf_counter()
     oracle.spmm(rv[:probe], ridx[:probe // lin.g], Xn, lin.K, lin.n, lin.m, lin.g, cores)
     t_probe = time.perf_counter() - t0
     rows = int(args.cpu_seconds / max(t_probe, 1e-6) * probe) // lin.g * lin.g
     rows = max(lin.g, min(lin.M, rows))
-    t0 = time.perf_counter()
-    Yref, B = oracle.spmm(rv[:rows], ridx[:rows // lin.g], Xn, lin.K, lin.n, lin.m, lin.g, cores)
-    t_spmm = time.perf_counter() - t0
-    flop = 2 * lin.N * rows * L.C * L.n
-    # spot check of the GPU packing and product on the sample
-    nmg_compress_ok = bool(np.array_equal(idx.cpu().numpy(), ridx))
+    # repeat a short sample until about a second of work has been timed
+    reps, t_spmm = 0, 0.0
+    while reps == 0 or (t_spmm < 1.0 and reps < 20):
+        t0 = time.perf_counter()
+        Yref, B = oracle.spmm(rv[:rows], ridx[:rows // lin.g], Xn, lin.K, lin.n, lin.m, lin.g,
+                              cores)
+        t_spmm += time.perf_counter() - t0
+        reps += 1
+    flop = 2 * lin.N * rows * L.C * L.n * reps
+    ok = bool(np.array_equal(idx.cpu().numpy(), ridx))
     Yg = Y[:rows].cpu().numpy().astype(np.float64)
-    prod_ok = bool((np.abs(Yg - Yref) <= 1e-5 * B).all())
+    tol = 1e-5 if lin.dtype.itemsize == 4 else 2e-2
+    ok = ok and bool((np.abs(Yg - Yref) <= tol * B).all())
     return {
         "value": round(flop / t_spmm / 1e9, 3),
         "unit": "GFLOP/s",
         "cores": cores,
         "kind": "oracle",
-        "sample": f"oracle compress of the full 3072x768 weight ({t_compress:.2f} s) and the "
-                  f"binary64 oracle product for the first {rows} of 3072 rows x 4096 tokens "
-                  f"({t_spmm:.2f} s, OpenMP over rows)",
-        "gpu_matches_sample": nmg_compress_ok and prod_ok,
+        "sample": f"oracle compress of the full {lin.M}x{lin.K} weight ({t_compress:.3f} s), then "
+                  f"the binary64 oracle product of the first {rows} of {lin.M} rows x {lin.N} "
+                  f"tokens, {reps} time(s) ({t_spmm:.2f} s, OpenMP over rows on {cores} threads)",
+        "gpu_matches_sample": ok,
     }
+
+
+def headline(ctx, args):
+    wl = ctx.synth.WORKLOADS[args.workload]
+    lin = wl.layers[0]
+    res = time_layer(ctx, args, args.workload, 0, lin, args.kernel)
+    rec = layer_record(lin, res)
+    if args.workload == 2:
+        rec["roofline"]["traffic"] = stored_traffic(source_digest())
+    out = {
+        "metric": METRIC if args.workload == 2 else "nmg_spmm useful GFLOP/s",
+        "value": round(lin.useful_flop / (res["ms_step"] * 1e-3) / 1e9, 1),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(res["ms_step"], 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if lin.dtype.itemsize == 4 else "f16",
+        "data": "synthetic",
+        "config": {"workload": wl.key, "M": lin.M, "K": lin.K, "N": lin.N, "n": lin.n,
+                   "m": lin.m, "g": lin.g, "kernel": res["kernel"],
+                   "rotated_sets": res["n_sets"], "step": "nmg_compress + nmg_spmm"},
+        **rec,
+        "wall_s_timed": round(res["wall"], 4),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args, lin, res["L"], res["sets"][0])
+    print(json.dumps(out), flush=True)
+
+
+def sweep(ctx, args):
+    for j, lin in enumerate(ctx.synth.SWEEP.layers):
+        res = time_layer(ctx, args, 5, j, lin, args.kernel)
+        rec = layer_record(lin, res)
+        W, v = res["sets"][0][0], res["sets"][0][2]
+        energy = float(v.double().abs().sum() / W.double().abs().sum())
+        print(json.dumps({"metric": "nmg_spmm useful GFLOP/s", "point": lin.name,
+                          "value": rec["spmm_gflops"], "unit": "GFLOP/s",
+                          "kernel": res["kernel"], "energy": round(energy, 4),
+                          "ms_per_step": round(res["ms_step"], 5), **rec}), flush=True)
+        del res
+
+
+def stack(ctx, args):
+    """Forward of the 12-layer fp16 linear stack (48 sparse products, 12 GELU,
+    24 residual sums), weights compressed once beforehand."""
+    torch, nmg, synth = ctx.torch, ctx.nmg, ctx.synth
+    from paper_2304_07613_amd.stack import LinearStack
+    st = LinearStack.from_workload(4, nmg, keep_dense=False)
+    torch.cuda.synchronize()
+    x = synth.normal((synth.BERT_HIDDEN, synth.BERT_TOKENS), synth.seed_for(4, 0, "X"), 1.0,
+                     torch.float16).to(ctx.dev)
+    for _ in range(max(1, args.warmup // 5)):
+        st.forward(x)
+    torch.cuda.synchronize()
+    reps = max(1, args.steps // 20)
+    a, b = ctx.event(), ctx.event()
+    a.record(ctx.stream)
+    for _ in range(reps):
+        y = st.forward(x)
+    b.record(ctx.stream)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    flop = 12 * sum(l.useful_flop for l in synth.bert_stack_layers())
+    print(json.dumps({"metric": "BERT-base linear stack forward, useful GFLOP/s",
+                      "value": round(flop / (ms * 1e-3) / 1e9, 1), "unit": "GFLOP/s",
+                      "ms_per_forward": round(ms, 4),
+                      "tokens_per_s": round(synth.BERT_TOKENS / (ms * 1e-3), 1),
+                      "dtype": "f16 (binary32 accumulate)", "layers": 12, "reps": reps,
+                      "finite": bool(torch.isfinite(y.float()).all())}), flush=True)
+
+
+def copy_calibration(ctx, args):
+    """A plain device-to-device copy of known size (torch's copy kernel),
+    256 MiB per launch over rotating buffers, for scaling FETCH_SIZE and
+    WRITE_SIZE."""
+    torch = ctx.torch
+    nbytes = 256 << 20
+    bufs = [torch.empty(nbytes // 4, dtype=torch.float32, device=ctx.dev).fill_(1.0)
+            for _ in range(8)]
+    torch.cuda.synchronize()
+    a, b = ctx.event(), ctx.event()
+    reps = 8
+    a.record(ctx.stream)
+    for r in range(reps):
+        bufs[(2 * r + 1) % 8].copy_(bufs[(2 * r) % 8])
+    b.record(ctx.stream)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    print(json.dumps({"mode": "copy-calibration", "bytes_read_per_copy": nbytes,
+                      "bytes_written_per_copy": nbytes, "copies": reps,
+                      "ms_per_copy": round(ms, 4),
+                      "gbs_read_plus_write": round(2 * nbytes / (ms * 1e-3) / 1e9, 1)}),
+          flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: this build "
+              f"runs on a single GPU (the product shards by tokens with no communication)",
+              file=sys.stderr)
+        sys.exit(2)
+    ctx = Ctx()
+    if args.copy_calibration:
+        copy_calibration(ctx, args)
+    elif args.sweep:
+        sweep(ctx, args)
+    elif args.stack:
+        stack(ctx, args)
+    else:
+        headline(ctx, args)
 
 
 if __name__ == "__main__":
