@@ -24,7 +24,6 @@ from __future__ import annotations
 
 import argparse
 import ctypes
-import hashlib
 import json
 import os
 import re
@@ -40,6 +39,8 @@ HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, GB/s
 FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense binary32 matrix peak
 FP32_VALU_PEAK_TFLOPS = 78.6    # binary32 vector FMA without packed math (2 FLOP/lane/clk)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "spmm_bert-ffn-up_traffic.txt")
+KERNEL_SYMBOL = {"mfma_scalar": "k_spmm_mfma_s", "mfma_general": "k_spmm_mfma",
+                 "valu": "k_spmm_valu"}
 
 
 def parse():
@@ -47,7 +48,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--kernel", choices=("auto", "mfma", "valu"), default="auto")
+    ap.add_argument("--kernel", choices=("auto", "mfma", "valu", "mfma_general", "mfma_scalar"),
+                    default="auto")
     ap.add_argument("--workload", type=int, choices=(1, 2, 3), default=2)
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--stack", action="store_true")
@@ -63,8 +65,8 @@ def parse():
 
 
 def source_digest() -> str:
-    with open(os.path.join(ROOT, "paper_2304_07613_amd", "csrc", "nmg.hip"), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    from paper_2304_07613_amd import build
+    return build.source_digest()
 
 
 def stored_traffic(digest: str):
@@ -175,7 +177,7 @@ def family_times(ctx, L, sets, kernel, reps=20):
     the timed region): the evidence behind the automatic choice."""
     torch, nmg = ctx.torch, ctx.nmg
     out = {}
-    for fam in ("mfma", "valu"):
+    for fam in ("mfma_scalar", "mfma_general", "valu"):
         try:
             for r in range(3):
                 W, X, v, idx, Y = sets[r % len(sets)]
@@ -201,14 +203,13 @@ def layer_record(lin, res):
     kernel = res["kernel"]
     spmm_s = res["spmm_ms"] * 1e-3
     tflops = lin.useful_flop / spmm_s / 1e12
-    if kernel == "mfma":
-        peak = FP32_MFMA_PEAK_TFLOPS  # binary32 matrix cores for both input types
-    else:
-        peak = FP32_VALU_PEAK_TFLOPS
+    matrix = kernel.startswith("mfma")
+    # binary32 matrix cores for both input types; the vector kernel without packed math
+    peak = FP32_MFMA_PEAK_TFLOPS if matrix else FP32_VALU_PEAK_TFLOPS
     rec = {
         "roofline": {
-            "kernel": f"k_spmm_{kernel}",
-            "bound": "mfma" if kernel == "mfma" else "alu",
+            "kernel": KERNEL_SYMBOL.get(kernel, kernel),
+            "bound": "mfma" if matrix else "alu",
             "achieved": round(tflops, 2),
             "peak": peak,
             "unit": "TFLOP/s",

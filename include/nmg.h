@@ -81,13 +81,18 @@ typedef struct nmg_layout {
 
 /* Kernel family for the product (the choice is recorded, not guessed). */
 typedef enum nmg_kernel {
-    NMG_KERNEL_AUTO = 0,     /* the library's choice for this layout        */
-    NMG_KERNEL_VALU = 1,     /* vector-ALU FMA; runs every valid layout      */
-    NMG_KERNEL_MFMA = 2      /* binary32 matrix cores on the gathered g x n
-                                sub-tiles; needs g % 4 == 0 and n dividing
-                                16 with 16*m/n <= 128 (or a smaller power-of-
-                                two window that n divides), else
-                                NMG_ERR_UNSUPPORTED */
+    NMG_KERNEL_AUTO = 0,         /* the library's choice for this layout       */
+    NMG_KERNEL_VALU = 1,         /* vector-ALU FMA; runs every valid layout     */
+    NMG_KERNEL_MFMA = 2,         /* the best binary32 matrix-core kernel below
+                                    that takes this layout                      */
+    NMG_KERNEL_MFMA_GENERAL = 3, /* matrix cores on the gathered g x n sub-tiles;
+                                    needs g % 4 == 0 and a window of 2..16
+                                    k-slots (a power of two that n divides)
+                                    whose chunks fit its staging buffer         */
+    NMG_KERNEL_MFMA_SCALAR = 4   /* the same product with scalar-loaded indices
+                                    and wider token tiles; additionally needs n a
+                                    power of two, C*n % 4 == 0, 4-byte aligned
+                                    indices and a window of 4..16 k-slots      */
 } nmg_kernel;
 
 /* Checks 1 <= n <= m <= 255, g >= 1, M >= 1, K >= 1 (NMG_ERR_PARAM),
@@ -120,13 +125,16 @@ nmg_status nmg_spmm(const nmg_layout *layout, const void *values,
                     const uint8_t *indices, const void *X, int64_t ldx,
                     int64_t N, void *Y, int64_t ldy, hipStream_t stream);
 
-/* nmg_spmm with an explicit kernel family. */
+/* nmg_spmm with an explicit kernel family; NMG_ERR_UNSUPPORTED when that
+ * family cannot run this layout. */
 nmg_status nmg_spmm_with(const nmg_layout *layout, nmg_kernel kernel,
                          const void *values, const uint8_t *indices,
                          const void *X, int64_t ldx, int64_t N, void *Y,
                          int64_t ldy, hipStream_t stream);
 
-/* The kernel family NMG_KERNEL_AUTO picks for this layout and N. */
+/* The kernel family NMG_KERNEL_AUTO picks for this layout and N, assuming
+ * 4-byte aligned indices and ldx = N (never NMG_KERNEL_AUTO or
+ * NMG_KERNEL_MFMA; NMG_KERNEL_AUTO only for an invalid layout). */
 nmg_kernel nmg_spmm_auto_kernel(const nmg_layout *layout, int64_t N);
 
 /* n:m:g -> dense (end of Section 5.2): W_out (M x K, leading dimension

@@ -1,0 +1,184 @@
+// abi.hip -- the C ABI of libnmg (include/nmg.h): host-side validation and
+// dispatch to the kernels' launchers.  Nothing here touches the GPU except
+// through those launchers and two cached runtime queries.
+//
+// Paper: STen (arXiv 2304.07613), Section 5.
+#include "common.hpp"
+
+namespace nmg_internal {
+
+int device_cus() {
+    static std::atomic<int> cus{0};
+    int v = cus.load(std::memory_order_relaxed);
+    if (v > 0) return v;
+    int dev = 0, c = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || c < 1)
+        c = 256;
+    cus.store(c, std::memory_order_relaxed);
+    return c;
+}
+
+// Occupancy figures from the HIP runtime, cached in a fixed table keyed by
+// (kernel, threads); a lost race only repeats the query.
+int kernel_occupancy(const void *kernel, int threads) {
+    struct Entry {
+        std::atomic<const void *> kernel{nullptr};
+        std::atomic<int> threads{0};
+        std::atomic<int> occ{0};
+    };
+    static Entry table[512];
+    const size_t h = ((reinterpret_cast<uintptr_t>(kernel) >> 4) * 31 + (size_t)threads) % 512;
+    Entry &e = table[h];
+    if (e.kernel.load(std::memory_order_acquire) == kernel &&
+        e.threads.load(std::memory_order_acquire) == threads) {
+        const int v = e.occ.load(std::memory_order_acquire);
+        if (v > 0) return v;
+    }
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kernel, threads, 0) != hipSuccess || nb < 1)
+        nb = 1;
+    e.occ.store(0, std::memory_order_release);
+    e.kernel.store(kernel, std::memory_order_release);
+    e.threads.store(threads, std::memory_order_release);
+    e.occ.store(nb, std::memory_order_release);
+    return nb;
+}
+
+}  // namespace nmg_internal
+
+using namespace nmg_internal;
+
+extern "C" {
+
+nmg_status nmg_layout_init(nmg_layout *layout, int32_t M, int32_t K, int32_t n, int32_t m,
+                           int32_t g, nmg_dtype dtype) {
+    if (!layout) return NMG_ERR_NULL;
+    nmg_layout L;
+    L.M = M;
+    L.K = K;
+    L.n = n;
+    L.m = m;
+    L.g = g;
+    L.C = (m >= 1 && K >= 1) ? (K + m - 1) / m : 0;
+    L.dtype = dtype;
+    const nmg_status st = check_layout(&L);
+    if (st != NMG_OK) return st;
+    *layout = L;
+    return NMG_OK;
+}
+
+int64_t nmg_values_numel(const nmg_layout *layout) {
+    if (check_layout(layout) != NMG_OK) return -1;
+    return (int64_t)layout->M * layout->C * layout->n;
+}
+
+int64_t nmg_indices_numel(const nmg_layout *layout) {
+    if (check_layout(layout) != NMG_OK) return -1;
+    return (int64_t)(layout->M / layout->g) * layout->C * layout->n;
+}
+
+nmg_status nmg_compress(const nmg_layout *L, const void *W, int64_t ldw, void *values,
+                        uint8_t *indices, hipStream_t stream) {
+    nmg_status st = check_layout(L);
+    if (st != NMG_OK) return st;
+    if (!W || !values || !indices) return NMG_ERR_NULL;
+    if (ldw < L->K) return NMG_ERR_PARAM;
+    const size_t es = elem_size(L->dtype);
+    if (!aligned(W, es) || !aligned(values, es)) return NMG_ERR_ALIGN;
+    return launch_compress(L, W, ldw, values, indices, stream);
+}
+
+nmg_kernel nmg_spmm_auto_kernel(const nmg_layout *L, int64_t N) {
+    if (check_layout(L) != NMG_OK) return NMG_KERNEL_AUTO;
+    if (spmm_scalar_supported(L, nullptr, N)) return NMG_KERNEL_MFMA_SCALAR;
+    return spmm_general_supported(L, N) ? NMG_KERNEL_MFMA_GENERAL : NMG_KERNEL_VALU;
+}
+
+nmg_status nmg_spmm_with(const nmg_layout *L, nmg_kernel kernel, const void *values,
+                         const uint8_t *indices, const void *X, int64_t ldx, int64_t N, void *Y,
+                         int64_t ldy, hipStream_t stream) {
+    nmg_status st = check_layout(L);
+    if (st != NMG_OK) return st;
+    if (!values || !indices || !X || !Y) return NMG_ERR_NULL;
+    if (N < 1 || N > INT32_MAX || ldx < N || ldy < N) return NMG_ERR_PARAM;
+    const size_t es = elem_size(L->dtype);
+    if (!aligned(X, es) || !aligned(values, es) || !aligned(Y, es)) return NMG_ERR_ALIGN;
+    const SpmmArgs a{L, values, indices, X, ldx, (int)N, Y, ldy, stream};
+    const bool scalar_ok = spmm_scalar_supported(L, indices, ldx);
+    if (kernel == NMG_KERNEL_AUTO) {
+        kernel = scalar_ok                        ? NMG_KERNEL_MFMA_SCALAR
+                 : spmm_general_supported(L, N) ? NMG_KERNEL_MFMA_GENERAL
+                                                  : NMG_KERNEL_VALU;
+    } else if (kernel == NMG_KERNEL_MFMA) {
+        kernel = scalar_ok ? NMG_KERNEL_MFMA_SCALAR : NMG_KERNEL_MFMA_GENERAL;
+    }
+    switch (kernel) {
+        case NMG_KERNEL_MFMA_SCALAR:
+            return scalar_ok ? spmm_scalar(a) : NMG_ERR_UNSUPPORTED;
+        case NMG_KERNEL_MFMA_GENERAL:
+            if (!spmm_general_supported(L, N)) return NMG_ERR_UNSUPPORTED;
+            return L->dtype == NMG_F32 ? spmm_general_f32(a) : spmm_general_f16(a);
+        case NMG_KERNEL_VALU:
+            return spmm_valu(a);
+        default:
+            return NMG_ERR_PARAM;
+    }
+}
+
+nmg_status nmg_spmm(const nmg_layout *L, const void *values, const uint8_t *indices,
+                    const void *X, int64_t ldx, int64_t N, void *Y, int64_t ldy,
+                    hipStream_t stream) {
+    return nmg_spmm_with(L, NMG_KERNEL_AUTO, values, indices, X, ldx, N, Y, ldy, stream);
+}
+
+nmg_status nmg_densify(const nmg_layout *L, const void *values, const uint8_t *indices,
+                       void *W_out, int64_t ldw, hipStream_t stream) {
+    nmg_status st = check_layout(L);
+    if (st != NMG_OK) return st;
+    if (!values || !indices || !W_out) return NMG_ERR_NULL;
+    if (ldw < L->K) return NMG_ERR_PARAM;
+    const size_t es = elem_size(L->dtype);
+    if (!aligned(values, es) || !aligned(W_out, es)) return NMG_ERR_ALIGN;
+    return launch_densify(L, values, indices, W_out, ldw, stream);
+}
+
+nmg_status nmg_gelu(nmg_dtype dtype, const void *in, void *out, int64_t count,
+                    hipStream_t stream) {
+    if (dtype != NMG_F32 && dtype != NMG_F16) return NMG_ERR_DTYPE;
+    if (!in || !out) return NMG_ERR_NULL;
+    if (count < 0) return NMG_ERR_PARAM;
+    if (count == 0) return NMG_OK;
+    const size_t es = elem_size(dtype);
+    if (!aligned(in, es) || !aligned(out, es)) return NMG_ERR_ALIGN;
+    return launch_gelu(dtype, in, out, count, stream);
+}
+
+nmg_status nmg_add(nmg_dtype dtype, const void *a, const void *b, void *out, int64_t count,
+                   hipStream_t stream) {
+    if (dtype != NMG_F32 && dtype != NMG_F16) return NMG_ERR_DTYPE;
+    if (!a || !b || !out) return NMG_ERR_NULL;
+    if (count < 0) return NMG_ERR_PARAM;
+    if (count == 0) return NMG_OK;
+    const size_t es = elem_size(dtype);
+    if (!aligned(a, es) || !aligned(b, es) || !aligned(out, es)) return NMG_ERR_ALIGN;
+    return launch_add(dtype, a, b, out, count, stream);
+}
+
+const char *nmg_status_str(nmg_status s) {
+    switch (s) {
+        case NMG_OK: return "ok";
+        case NMG_ERR_NULL: return "null pointer";
+        case NMG_ERR_PARAM: return "invalid parameter";
+        case NMG_ERR_SHAPE: return "invalid shape";
+        case NMG_ERR_DTYPE: return "unknown dtype";
+        case NMG_ERR_ALIGN: return "misaligned pointer or leading dimension";
+        case NMG_ERR_LAUNCH: return "kernel launch failed";
+        case NMG_ERR_UNSUPPORTED: return "kernel does not support this layout";
+    }
+    return "unknown status";
+}
+
+const char *nmg_version(void) { return "nmg 0.2.0 gfx950"; }
+
+}  // extern "C"

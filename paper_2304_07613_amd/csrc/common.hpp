@@ -1,0 +1,171 @@
+// common.hpp -- shared by the translation units of libnmg: host-side helpers
+// and the internal launcher interface (namespace nmg_internal), and device
+// helpers (one private copy per translation unit).
+//
+// Paper: STen (arXiv 2304.07613), Section 5.  The layout, selection rule and
+// product are specified in include/nmg.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <atomic>
+#include <type_traits>
+#include <utility>
+
+#include "nmg.h"
+
+namespace nmg_internal {
+
+inline nmg_status check_layout(const nmg_layout *L) {
+    if (!L) return NMG_ERR_NULL;
+    if (L->dtype != NMG_F32 && L->dtype != NMG_F16) return NMG_ERR_DTYPE;
+    if (L->M < 1 || L->K < 1 || L->n < 1 || L->m < L->n || L->m > 255 || L->g < 1)
+        return NMG_ERR_PARAM;
+    if (L->M % L->g != 0) return NMG_ERR_SHAPE;
+    const int32_t C = (L->K + L->m - 1) / L->m;
+    if (L->C != C) return NMG_ERR_PARAM;
+    if (L->K - (C - 1) * L->m < L->n) return NMG_ERR_SHAPE;
+    return NMG_OK;
+}
+
+inline size_t elem_size(nmg_dtype d) { return d == NMG_F32 ? 4 : 2; }
+
+inline bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// X rows start on 4-element boundaries: four tokens come in one vector load.
+inline bool x_vectorisable(const nmg_layout *L, const void *X, int64_t ldx) {
+    return aligned(X, 4 * elem_size(L->dtype)) && ldx % 4 == 0;
+}
+
+inline nmg_status launched() {
+    return hipGetLastError() == hipSuccess ? NMG_OK : NMG_ERR_LAUNCH;
+}
+
+// Rows per group unit of the matrix-core kernels: the largest of 32, 16, 8,
+// 4 that divides g; 0 if g % 4 != 0.
+inline int mfma_unit(const nmg_layout *L) {
+    for (int u = 32; u >= 4; u /= 2)
+        if (L->g % u == 0) return u;
+    return 0;
+}
+
+// Compute units of the current device (cached), and workgroups of `kernel`
+// with `threads` threads that fit one of them (cached per kernel and size).
+int device_cus();
+int kernel_occupancy(const void *kernel, int threads);
+
+// One product launch: arguments validated by the C ABI.
+struct SpmmArgs {
+    const nmg_layout *L;
+    const void *values;
+    const uint8_t *indices;
+    const void *X;
+    int64_t ldx;
+    int N;
+    void *Y;
+    int64_t ldy;
+    hipStream_t stream;
+};
+
+nmg_status launch_compress(const nmg_layout *L, const void *W, int64_t ldw, void *values,
+                           uint8_t *indices, hipStream_t stream);
+nmg_status launch_densify(const nmg_layout *L, const void *values, const uint8_t *indices,
+                          void *W_out, int64_t ldw, hipStream_t stream);
+nmg_status launch_gelu(nmg_dtype dtype, const void *in, void *out, int64_t count,
+                       hipStream_t stream);
+nmg_status launch_add(nmg_dtype dtype, const void *a, const void *b, void *out, int64_t count,
+                      hipStream_t stream);
+
+nmg_status spmm_valu(const SpmmArgs &a);
+
+bool spmm_general_supported(const nmg_layout *L, int64_t N);
+nmg_status spmm_general_f32(const SpmmArgs &a);
+nmg_status spmm_general_f16(const SpmmArgs &a);
+
+bool spmm_scalar_supported(const nmg_layout *L, const uint8_t *indices, int64_t ldx);
+nmg_status spmm_scalar(const SpmmArgs &a);
+nmg_status spmm_scalar_f32_u16(const SpmmArgs &a);
+nmg_status spmm_scalar_f32_u8(const SpmmArgs &a);
+nmg_status spmm_scalar_f32_u4(const SpmmArgs &a);
+nmg_status spmm_scalar_f16(const SpmmArgs &a);
+
+}  // namespace nmg_internal
+
+namespace {
+
+using namespace nmg_internal;
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+
+constexpr int kBlock = 256;  // threads per workgroup for every kernel
+
+template <typename T> struct Bits;
+template <> struct Bits<float> { using type = uint32_t; };
+template <> struct Bits<_Float16> { using type = uint16_t; };
+
+template <int... S, typename F>
+__device__ __forceinline__ void static_for_impl(std::integer_sequence<int, S...>, F &&f) {
+    (f(std::integral_constant<int, S>{}), ...);
+}
+// f(std::integral_constant<int, s>) for s = 0 .. N-1, fully unrolled.
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    static_for_impl(std::make_integer_sequence<int, N>{}, f);
+}
+
+// Four consecutive elements of row `p` (token t .. t+3) widened to binary32;
+// entries at or beyond `valid` are zero.  `vec` (uniform) says p is aligned to
+// four elements, so one vector load serves.
+template <typename T>
+__device__ __forceinline__ v4f load4(const T *p, int valid, bool vec) {
+    v4f v = {0.f, 0.f, 0.f, 0.f};
+    if (vec && valid >= 4) {
+        if constexpr (std::is_same<T, float>::value) {
+            v = *reinterpret_cast<const v4f *>(p);
+        } else {
+            h4 h = *reinterpret_cast<const h4 *>(p);
+            v = v4f{(float)h[0], (float)h[1], (float)h[2], (float)h[3]};
+        }
+    } else {
+        for (int j = 0; j < 4; ++j)
+            if (j < valid) v[j] = (float)p[j];
+    }
+    return v;
+}
+
+// XCD-aware tile order.  Workgroups are dealt round-robin to the 8 XCDs
+// (workgroup i runs on XCD i % 8); this maps them so that each XCD receives
+// one contiguous range of logical tiles, in which the row tiles of a token
+// tile are adjacent and share that token tile's X rows in the XCD's L2.
+__device__ __forceinline__ int xcd_tile(int i, int total) {
+    constexpr int kXcd = 8;
+    const int per = total / kXcd, rem = total % kXcd;
+    const int x = i % kXcd, j = i / kXcd;
+    return x * per + (x < rem ? x : rem) + j;
+}
+
+// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane
+// (global_load_lds_dwordx4; `lds` must be wave-uniform).  The builtin exists
+// only in the device pass.
+__device__ __forceinline__ void lds_copy16(const float *src, float *lds) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
+#else
+    (void)src;
+    (void)lds;
+#endif
+}
+
+// Wait for every outstanding memory operation of this wave.
+__device__ __forceinline__ void wait_all_memory() {
+#if defined(__HIP_DEVICE_COMPILE__)
+    __builtin_amdgcn_s_waitcnt(0);
+#endif
+}
+
+constexpr int ilog2(int v) { return v <= 1 ? 0 : 1 + ilog2(v / 2); }
+
+}  // namespace

@@ -1,0 +1,177 @@
+// k_elementwise.hip -- dense -> n:m:g (Section 5.2), n:m:g -> dense, and the
+// elementwise glue of the linear stack.
+//
+//   k_compress  one thread per column of a chunk-block: binary32 group score
+//               down the g rows (coalesced across lanes), rank by counting
+//               inside the chunk through LDS, then a coalesced copy of the
+//               kept weights.  HBM-bound.
+//   k_densify   one thread per output element.
+//   k_gelu, k_add
+#include "common.hpp"
+
+namespace {
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_compress(
+    const T *__restrict__ W, int64_t ldw, T *__restrict__ values,
+    uint8_t *__restrict__ indices, int K, int n, int m, int g, int C, int cpb) {
+    using B = typename Bits<T>::type;
+    __shared__ uint32_t key[kBlock];
+    __shared__ uint8_t keep[kBlock];
+    __shared__ uint8_t sel[kBlock];
+
+    const int G = blockIdx.x;                 // group
+    const int c_first = blockIdx.y * cpb;     // first chunk of this block
+    const int t = threadIdx.x;
+    const int lc = t / m, o = t - lc * m;     // local chunk, in-chunk offset
+    const int c = c_first + lc;
+    const bool in_block = lc < cpb && c < C;
+    const int w = in_block ? min(m, K - c * m) : 0;
+    const bool active = in_block && o < w;
+    const int64_t ldv = (int64_t)C * n;
+    const int64_t row0 = (int64_t)G * g;
+
+    // group score, binary32, rows in ascending order
+    uint32_t kk = 0;
+    if (active) {
+        const T *p = W + row0 * ldw + (int64_t)c * m + o;
+        float s = 0.0f;
+        for (int i = 0; i < g; ++i) s = s + fabsf((float)p[(int64_t)i * ldw]);
+        // scores are >= +0 or NaN: as unsigned integers the bit patterns of
+        // non-negative floats sort like the floats; NaNs become one value
+        // above +inf
+        kk = __builtin_isnan(s) ? 0x7fc00000u : __float_as_uint(s);
+    }
+    key[t] = kk;
+    __syncthreads();
+
+    // keep iff fewer than n columns of the chunk rank above this one
+    bool kp = false;
+    if (active) {
+        const int base = lc * m;
+        int rank = 0;
+        for (int i = 0; i < w; ++i) {
+            const uint32_t ki = key[base + i];
+            rank += (ki > kk) || (i < o && ki == kk);
+        }
+        kp = rank < n;
+    }
+    keep[t] = kp;
+    __syncthreads();
+
+    if (kp) {
+        const int base = lc * m;
+        int slot = 0;
+        for (int i = 0; i < o; ++i) slot += keep[base + i];
+        indices[(int64_t)G * ldv + (int64_t)c * n + slot] = (uint8_t)o;
+        sel[lc * n + slot] = (uint8_t)o;
+    }
+    __syncthreads();
+
+    // copy the kept weights of the g rows, bit for bit, coalesced on output
+    const int nout = min(cpb, C - c_first) * n;
+    for (int i = 0; i < g; ++i) {
+        const B *src = reinterpret_cast<const B *>(W + (row0 + i) * ldw);
+        B *dst = reinterpret_cast<B *>(values + (row0 + i) * ldv) + (int64_t)c_first * n;
+        for (int p = t; p < nout; p += kBlock) {
+            const int cc = c_first + p / n;
+            dst[p] = src[(int64_t)cc * m + sel[p]];
+        }
+    }
+}
+
+// ------------------------------------------------------------------ densify
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_densify(
+    const T *__restrict__ values, const uint8_t *__restrict__ indices,
+    T *__restrict__ out, int64_t ldw, int K, int n, int m, int g, int C) {
+    using B = typename Bits<T>::type;
+    const int64_t r = blockIdx.x;
+    const int k = blockIdx.y * kBlock + threadIdx.x;
+    if (k >= K) return;
+    const int c = k / m, o = k - c * m;
+    const int64_t ldv = (int64_t)C * n;
+    const uint8_t *idx = indices + (r / g) * ldv + (int64_t)c * n;
+    B v = 0;
+    for (int s = 0; s < n; ++s)
+        if (idx[s] == o) v = reinterpret_cast<const B *>(values)[r * ldv + (int64_t)c * n + s];
+    reinterpret_cast<B *>(out)[r * ldw + k] = v;
+}
+
+// ------------------------------------------------------------- elementwise
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_gelu(const T *in, T *out, int64_t count) {
+    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (i >= count) return;
+    const float x = (float)in[i];
+    // 1 + erf(z) written as erfc(-z): no cancellation for negative x
+    out[i] = (T)(0.5f * x * erfcf(-x * 0.70710678118654752f));
+}
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_add(const T *a, const T *b, T *out, int64_t count) {
+    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (i >= count) return;
+    out[i] = (T)((float)a[i] + (float)b[i]);
+}
+
+}  // namespace
+
+namespace nmg_internal {
+
+nmg_status launch_compress(const nmg_layout *L, const void *W, int64_t ldw, void *values,
+                           uint8_t *indices, hipStream_t stream) {
+    const int cpb = kBlock / L->m;  // chunks per block, >= 1 since m <= 255
+    dim3 grid(L->M / L->g, (L->C + cpb - 1) / cpb);
+    if (L->dtype == NMG_F32)
+        hipLaunchKernelGGL((k_compress<float>), grid, dim3(kBlock), 0, stream, (const float *)W, ldw,
+                           (float *)values, indices, L->K, L->n, L->m, L->g, L->C, cpb);
+    else
+        hipLaunchKernelGGL((k_compress<_Float16>), grid, dim3(kBlock), 0, stream,
+                           (const _Float16 *)W, ldw, (_Float16 *)values, indices, L->K, L->n, L->m,
+                           L->g, L->C, cpb);
+    return launched();
+}
+
+nmg_status launch_densify(const nmg_layout *L, const void *values, const uint8_t *indices,
+                          void *W_out, int64_t ldw, hipStream_t stream) {
+    dim3 grid(L->M, (L->K + kBlock - 1) / kBlock);
+    if (L->dtype == NMG_F32)
+        hipLaunchKernelGGL((k_densify<float>), grid, dim3(kBlock), 0, stream, (const float *)values,
+                           indices, (float *)W_out, ldw, L->K, L->n, L->m, L->g, L->C);
+    else
+        hipLaunchKernelGGL((k_densify<_Float16>), grid, dim3(kBlock), 0, stream,
+                           (const _Float16 *)values, indices, (_Float16 *)W_out, ldw, L->K, L->n,
+                           L->m, L->g, L->C);
+    return launched();
+}
+
+nmg_status launch_gelu(nmg_dtype dtype, const void *in, void *out, int64_t count,
+                       hipStream_t stream) {
+    const int64_t blocks = (count + kBlock - 1) / kBlock;
+    if (blocks > INT32_MAX) return NMG_ERR_PARAM;
+    if (dtype == NMG_F32)
+        hipLaunchKernelGGL((k_gelu<float>), dim3((unsigned)blocks), dim3(kBlock), 0, stream,
+                           (const float *)in, (float *)out, count);
+    else
+        hipLaunchKernelGGL((k_gelu<_Float16>), dim3((unsigned)blocks), dim3(kBlock), 0, stream,
+                           (const _Float16 *)in, (_Float16 *)out, count);
+    return launched();
+}
+
+nmg_status launch_add(nmg_dtype dtype, const void *a, const void *b, void *out, int64_t count,
+                      hipStream_t stream) {
+    const int64_t blocks = (count + kBlock - 1) / kBlock;
+    if (blocks > INT32_MAX) return NMG_ERR_PARAM;
+    if (dtype == NMG_F32)
+        hipLaunchKernelGGL((k_add<float>), dim3((unsigned)blocks), dim3(kBlock), 0, stream,
+                           (const float *)a, (const float *)b, (float *)out, count);
+    else
+        hipLaunchKernelGGL((k_add<_Float16>), dim3((unsigned)blocks), dim3(kBlock), 0, stream,
+                           (const _Float16 *)a, (const _Float16 *)b, (_Float16 *)out, count);
+    return launched();
+}
+
+}  // namespace nmg_internal

@@ -64,11 +64,15 @@ def test_calls_reject_bad_arguments_before_launch(lib):
     assert lib.nmg_compress(ctypes.byref(bad), p, 64, p, p, s) == nmg.ERR_PARAM
     # g % 4 != 0: the matrix-core kernel declines, the vector kernel is the choice
     assert lib.nmg_layout_init(ctypes.byref(L), 64, 64, 1, 4, 2, nmg.F32) == nmg.OK
-    assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS["mfma"], p, p, p, 32, 32, p, 32,
-                             s) == nmg.ERR_UNSUPPORTED
+    for fam in ("mfma", "mfma_general", "mfma_scalar"):
+        assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS[fam], p, p, p, 32, 32, p, 32,
+                                 s) == nmg.ERR_UNSUPPORTED
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 32) == nmg.KERNELS["valu"]
     assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 1, 4, 8, nmg.F32) == nmg.OK
-    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma"]
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_scalar"]
+    # C * n = 77 is not a multiple of 4: the general matrix-core kernel
+    assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 1, 10, 8, nmg.F32) == nmg.OK
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_general"]
 
 
 def test_status_strings(lib):
