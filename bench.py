@@ -11,8 +11,11 @@ distinct buffer sets (> 1 GB in total) that the 256 MB Infinity Cache cannot
 serve a step from the previous visit.
 
 Default output: ONE JSON line.  `value` = useful GFLOP (2 N nnz of the sparse
-weight) per step / step time; `roofline` describes nmg_spmm, the dominant
-kernel, from HIP events around each of its launches in the timed region;
+weight) per step / step time, from K whole steps launched back to back with
+HIP events only at the two ends.  `roofline` describes nmg_spmm, the dominant
+kernel: its average launch duration is measured with HIP events around K
+back-to-back launches of it alone over the same rotated sets (events between
+every kernel would themselves add several microseconds of idle per launch).
 `cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
 
 Other modes (not the headline): --workload 1|3 (the other single layers),
@@ -143,28 +146,38 @@ def time_layer(ctx, args, workload, layer_no, lin, kernel_req):
     torch.cuda.synchronize()
 
     K = args.steps
-    ev = [[ctx.event() for _ in range(3)] for _ in range(K)]
+    # (1) the timed region: K whole steps back to back, events only at its ends
     start, stop = ctx.event(), ctx.event()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     start.record(ctx.stream)
     for s in range(K):
         ca, sa = calls[s % n_sets]
-        ev[s][0].record(ctx.stream)
         status.append(compress_c(*ca))
-        ev[s][1].record(ctx.stream)
         status.append(spmm_c(*sa))
-        ev[s][2].record(ctx.stream)
     stop.record(ctx.stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    # (2) each kernel's average launch duration: K launches of it alone, back to
+    # back over the same rotated sets, between two events (launch gaps included)
+    def kernel_ms(which):
+        e0, e1 = ctx.event(), ctx.event()
+        e0.record(ctx.stream)
+        for s in range(K):
+            ca, sa = calls[s % n_sets]
+            status.append(compress_c(*ca) if which == 0 else spmm_c(*sa))
+        e1.record(ctx.stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / K
+    compress_ms = kernel_ms(0)
+    spmm_ms = kernel_ms(1)
     if any(status):
         raise nmg.NmgError(next(x for x in status if x), "timed step")
     res = {
         "L": L, "kernel": kernel, "n_sets": n_sets, "sets": sets, "wall": wall,
         "ms_step": start.elapsed_time(stop) / K,
-        "compress_ms": sum(e[0].elapsed_time(e[1]) for e in ev) / K,
-        "spmm_ms": sum(e[1].elapsed_time(e[2]) for e in ev) / K,
+        "compress_ms": compress_ms,
+        "spmm_ms": spmm_ms,
         "bytes": nb,
     }
     if not args.no_family:

@@ -80,6 +80,86 @@ __global__ __launch_bounds__(kBlock) void k_compress(
     }
 }
 
+// --------------------------------------------------- compress, thread per chunk
+
+// For m <= MT (MT = 4, 8, 16 or 32): one thread owns one (group, chunk).  It
+// reads the chunk's m columns down the g rows (one vector load per row when
+// the chunk starts on a 16-byte boundary), sums the scores in binary32 in row
+// order, ranks them in registers (the same order as k_compress: key bits,
+// ties to the lower offset), and writes the indices and the kept weights of
+// the g rows.  Adjacent threads own adjacent chunks, so every load and store
+// is coalesced across the wave, and W is read exactly once.
+template <typename T, int MT>
+__global__ __launch_bounds__(kBlock) void k_compress_chunk(
+    const T *__restrict__ W, int64_t ldw, T *__restrict__ values,
+    uint8_t *__restrict__ indices, int K, int n, int m, int g, int C, bool vec) {
+    using B = typename Bits<T>::type;
+    constexpr int VB = 16 / sizeof(T);            // elements per 16-byte vector
+    const int G = blockIdx.x;
+    const int c = blockIdx.y * kBlock + threadIdx.x;
+    if (c >= C) return;
+    const int w = min(m, K - c * m);              // chunk width
+    const int64_t ldv = (int64_t)C * n;
+    const int64_t row0 = (int64_t)G * g;
+    const int64_t col0 = (int64_t)c * m;
+
+    float score[MT];
+#pragma unroll
+    for (int j = 0; j < MT; ++j) score[j] = 0.0f;
+    for (int i = 0; i < g; ++i) {
+        const T *p = W + (row0 + i) * ldw + col0;
+        if (vec && w == m) {
+            // m % VB == 0 here: whole 16-byte vectors
+#pragma unroll
+            for (int v = 0; v < MT / VB + (MT % VB != 0); ++v) {
+                if (v * VB < m) {
+                    typedef B BV __attribute__((ext_vector_type(VB)));
+                    const BV bits = *reinterpret_cast<const BV *>(p + v * VB);
+#pragma unroll
+                    for (int e = 0; e < VB; ++e) {
+                        const int j = v * VB + e;
+                        if (j < MT) {
+                            const B be = bits[e];
+                            score[j] = score[j] + fabsf((float)__builtin_bit_cast(T, be));
+                        }
+                    }
+                }
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < MT; ++j)
+                if (j < w) score[j] = score[j] + fabsf((float)p[j]);
+        }
+    }
+    // order keys: non-negative floats order like their bits; NaN above +inf
+    uint32_t key[MT];
+#pragma unroll
+    for (int j = 0; j < MT; ++j)
+        key[j] = __builtin_isnan(score[j]) ? 0x7fc00000u : __float_as_uint(score[j]);
+    int slot = 0;
+    uint8_t sel[MT];
+#pragma unroll
+    for (int j = 0; j < MT; ++j) {
+        if (j < w) {
+            int rank = 0;
+#pragma unroll
+            for (int i = 0; i < MT; ++i)
+                if (i < w) rank += (key[i] > key[j]) || (i < j && key[i] == key[j]);
+            if (rank < n) {
+                sel[slot < MT ? slot : 0] = (uint8_t)j;
+                ++slot;
+            }
+        }
+    }
+    uint8_t *ip = indices + (int64_t)G * ldv + (int64_t)c * n;
+    for (int s = 0; s < n; ++s) ip[s] = sel[s];
+    for (int i = 0; i < g; ++i) {
+        const B *src = reinterpret_cast<const B *>(W + (row0 + i) * ldw + col0);
+        B *dst = reinterpret_cast<B *>(values + (row0 + i) * ldv) + (int64_t)c * n;
+        for (int s = 0; s < n; ++s) dst[s] = src[sel[s]];
+    }
+}
+
 // ------------------------------------------------------------------ densify
 
 template <typename T>
@@ -121,8 +201,32 @@ __global__ __launch_bounds__(kBlock) void k_add(const T *a, const T *b, T *out, 
 
 namespace nmg_internal {
 
+template <typename T>
+nmg_status launch_compress_chunk(const nmg_layout *L, const void *W, int64_t ldw, void *values,
+                                 uint8_t *indices, hipStream_t stream) {
+    const bool vec = aligned(W, 16) && (ldw * sizeof(T)) % 16 == 0 &&
+                     (L->m * sizeof(T)) % 16 == 0;
+    dim3 grid(L->M / L->g, (L->C + kBlock - 1) / kBlock);
+#define NMG_CHUNK(MT)                                                                          \
+    hipLaunchKernelGGL((k_compress_chunk<T, MT>), grid, dim3(kBlock), 0, stream, (const T *)W,   \
+                       ldw, (T *)values, indices, L->K, L->n, L->m, L->g, L->C, vec)
+    if (L->m <= 4) NMG_CHUNK(4);
+    else if (L->m <= 8) NMG_CHUNK(8);
+    else if (L->m <= 16) NMG_CHUNK(16);
+    else NMG_CHUNK(32);
+#undef NMG_CHUNK
+    return launched();
+}
+
 nmg_status launch_compress(const nmg_layout *L, const void *W, int64_t ldw, void *values,
                            uint8_t *indices, hipStream_t stream) {
+    // up to 32 columns per chunk and enough (group, chunk) pairs to fill the
+    // GPU: one thread per chunk, in registers; otherwise one thread per column
+    const int64_t pairs = (int64_t)(L->M / L->g) * L->C;
+    if (L->m <= 32 && pairs >= 65536)
+        return L->dtype == NMG_F32
+                   ? launch_compress_chunk<float>(L, W, ldw, values, indices, stream)
+                   : launch_compress_chunk<_Float16>(L, W, ldw, values, indices, stream);
     const int cpb = kBlock / L->m;  // chunks per block, >= 1 since m <= 255
     dim3 grid(L->M / L->g, (L->C + cpb - 1) / cpb);
     if (L->dtype == NMG_F32)

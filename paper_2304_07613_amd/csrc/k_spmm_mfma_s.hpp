@@ -15,9 +15,15 @@ namespace {
 // feeds TPL*U/4 matrix instructions.
 constexpr int kFastRowsWave = 16;                  // 4 quads
 constexpr int kFastMaxWaves = 16;
-constexpr int kFastStageFloats = 8192;             // 32 KB per staging buffer, two buffers
+constexpr int kFastStageFloats = 16384;            // 64 KB per staging buffer, two buffers
+                                                   // (register staging: half of it)
 
-__host__ __device__ constexpr int fast_window_rows(int tpl) { return kFastStageFloats / (64 * tpl); }
+__host__ __device__ constexpr int fast_stage_floats(bool direct) {
+    return direct ? kFastStageFloats : kFastStageFloats / 2;
+}
+__host__ __device__ constexpr int fast_window_rows(int tpl, bool direct) {
+    return fast_stage_floats(direct) / (64 * tpl);
+}
 
 template <int TPL> struct TokVec4;
 template <> struct TokVec4<1> { typedef float type; };
@@ -42,14 +48,14 @@ __global__ __launch_bounds__(DIRECT ? 64 * kFastMaxWaves : 64 * kFastMaxWaves / 
     constexpr int QPU = U / 4;                    // quads per unit
     constexpr int TN = 64 * TPL;                  // tokens per workgroup
     constexpr int C4 = TN / 4;                    // 4-token vectors per staged row
-    constexpr int MAXR = fast_window_rows(TPL);   // staged rows per window, max
+    constexpr int MAXR = fast_window_rows(TPL, DIRECT);  // staged rows per window, max
     constexpr int RPI = 1024 / (4 * TN);          // rows per direct load instruction
     constexpr int CBSZ = ilog2(KSW);
     constexpr int IW = KSW / 4;                   // index words per unit and window
     constexpr int XVMAX = (MAXR * C4 + 4 * 64 - 1) / (4 * 64);  // register staging, >= 4 waves
     typedef typename TokVec4<TPL>::type BV;
-    __shared__ float xs0[kFastStageFloats];
-    __shared__ float xs1[kFastStageFloats];
+    __shared__ float xs0[fast_stage_floats(DIRECT)];
+    __shared__ float xs1[fast_stage_floats(DIRECT)];
 
     const int nthreads = blockDim.x;
     const int nwaves = nthreads >> 6;
@@ -261,10 +267,11 @@ __global__ __launch_bounds__(DIRECT ? 64 * kFastMaxWaves : 64 * kFastMaxWaves / 
 // ---------------------------------------------------- fast kernel selection
 
 // Largest window of 16, 8 or 4 k-slots that n divides and whose chunks fit
-// the fast kernel's staged rows; 0 if none.
-int fast_window(const nmg_layout *L, int tpl) {
+// the staged rows of the variant; 0 if none.  (The register-staged variant's
+// smaller budget decides whether the layout is taken at all.)
+int fast_window(const nmg_layout *L, int tpl, bool direct = false) {
     for (int ksw = 16; ksw >= 4; ksw /= 2)
-        if (ksw % L->n == 0 && (ksw / L->n) * L->m <= fast_window_rows(tpl)) return ksw;
+        if (ksw % L->n == 0 && (ksw / L->n) * L->m <= fast_window_rows(tpl, direct)) return ksw;
     return 0;
 }
 
@@ -323,7 +330,7 @@ nmg_status launch_fast_ut(const nmg_layout *L, const void *values, const uint8_t
                         L, values, indices, X, ldx, N, Y, ldy, xvec, stream)                    \
                   : launch_fast_v<T, U, KSW, TPL, false>(L, values, indices, X, ldx, N, Y, ldy, \
                                                          xvec, stream)
-    switch (fast_window(L, TPL)) {
+    switch (fast_window(L, TPL, direct)) {
         case 16: NMG_FAST(16);
         case 8: NMG_FAST(8);
         case 4: NMG_FAST(4);
