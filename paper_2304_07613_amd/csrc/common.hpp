@@ -150,9 +150,11 @@ __device__ __forceinline__ int xcd_tile(int i, int total) {
 // 16 bytes per lane from global memory straight into LDS at lds + 16 * lane
 // (global_load_lds_dwordx4; `lds` must be wave-uniform).  The builtin exists
 // only in the device pass.
-__device__ __forceinline__ void lds_copy16(const float *src, float *lds) {
+template <typename E>
+__device__ __forceinline__ void lds_copy16(const E *src, E *lds) {
 #if defined(__HIP_DEVICE_COMPILE__)
-    __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const float *>(src),
+                                     reinterpret_cast<float *>(lds), 16, 0, 0);
 #else
     (void)src;
     (void)lds;

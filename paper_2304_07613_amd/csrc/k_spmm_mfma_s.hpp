@@ -15,24 +15,23 @@ namespace {
 // feeds TPL*U/4 matrix instructions.
 constexpr int kFastRowsWave = 16;                  // 4 quads
 constexpr int kFastMaxWaves = 16;
-constexpr int kFastStageFloats = 16384;            // 64 KB per staging buffer, two buffers
-                                                   // (register staging: half of it)
-
-__host__ __device__ constexpr int fast_stage_floats(bool direct) {
-    return direct ? kFastStageFloats : kFastStageFloats / 2;
-}
-__host__ __device__ constexpr int fast_window_rows(int tpl, bool direct) {
-    return fast_stage_floats(direct) / (64 * tpl);
+// Staging buffers: 64 KB each when X is copied straight to LDS in its own
+// element type, 32 KB when it passes through registers (as binary32).
+__host__ __device__ constexpr int fast_stage_bytes(bool direct) { return direct ? 65536 : 32768; }
+// Staged X rows per window for a token tile of 64 * TPL elements of `es` bytes.
+__host__ __device__ constexpr int fast_window_rows(int tpl, bool direct, int es) {
+    return fast_stage_bytes(direct) / (64 * tpl * es);
 }
 
-template <int TPL> struct TokVec4;
-template <> struct TokVec4<1> { typedef float type; };
-template <> struct TokVec4<2> { typedef float type __attribute__((ext_vector_type(2))); };
-template <> struct TokVec4<4> { typedef float type __attribute__((ext_vector_type(4))); };
+// TPL consecutive staged elements (the tokens one lane multiplies).
+template <typename SE, int TPL> struct TokVec4 {
+    typedef SE type __attribute__((ext_vector_type(TPL)));
+};
+template <typename SE> struct TokVec4<SE, 1> { typedef SE type; };
 
-template <int TPL>
-__device__ __forceinline__ float tok_part4(const typename TokVec4<TPL>::type &v, int p) {
-    if constexpr (TPL == 1) { (void)p; return v; } else { return v[p]; }
+template <typename SE, int TPL>
+__device__ __forceinline__ float tok_part4(const typename TokVec4<SE, TPL>::type &v, int p) {
+    if constexpr (TPL == 1) { (void)p; return (float)v; } else { return (float)v[p]; }
 }
 
 template <typename T, int U, int KSW, int TPL, bool DIRECT>
@@ -41,21 +40,25 @@ __global__ __launch_bounds__(DIRECT ? 64 * kFastMaxWaves : 64 * kFastMaxWaves / 
     const T *__restrict__ X, int64_t ldx, T *__restrict__ Y, int64_t ldy,
     int M, int K, int N, int log2n, int m, int g, int C, int row_tiles, int tiles, bool xvec,
     bool yvec) {
-    static_assert(!DIRECT || std::is_same<T, float>::value, "direct staging copies binary32");
     static_assert(KSW % 4 == 0 && U <= kFastRowsWave, "window of whole index words");
+    // staged element: X's own type when copied directly, binary32 otherwise
+    typedef typename std::conditional<DIRECT, T, float>::type SE;
+    constexpr int SES = (int)sizeof(SE);
     constexpr int QW = kFastRowsWave / 4;         // quads per wave
     constexpr int UNITS = kFastRowsWave / U;      // group units per wave
     constexpr int QPU = U / 4;                    // quads per unit
     constexpr int TN = 64 * TPL;                  // tokens per workgroup
     constexpr int C4 = TN / 4;                    // 4-token vectors per staged row
-    constexpr int MAXR = fast_window_rows(TPL, DIRECT);  // staged rows per window, max
-    constexpr int RPI = 1024 / (4 * TN);          // rows per direct load instruction
+    constexpr int MAXR = fast_window_rows(TPL, DIRECT, SES);  // staged rows per window, max
+    constexpr int EPL = 16 / SES;                 // elements per lane of a direct copy
+    constexpr int LPR = TN / EPL;                 // lanes per staged row (direct copy)
+    constexpr int RPI = 64 / LPR;                 // rows per direct copy instruction (1 KB)
     constexpr int CBSZ = ilog2(KSW);
     constexpr int IW = KSW / 4;                   // index words per unit and window
     constexpr int XVMAX = (MAXR * C4 + 4 * 64 - 1) / (4 * 64);  // register staging, >= 4 waves
-    typedef typename TokVec4<TPL>::type BV;
-    __shared__ float xs0[fast_stage_floats(DIRECT)];
-    __shared__ float xs1[fast_stage_floats(DIRECT)];
+    typedef typename TokVec4<SE, TPL>::type BV;
+    __shared__ SE xs0[fast_stage_bytes(DIRECT) / SES];
+    __shared__ SE xs1[fast_stage_bytes(DIRECT) / SES];
 
     const int nthreads = blockDim.x;
     const int nwaves = nthreads >> 6;
@@ -119,19 +122,20 @@ __global__ __launch_bounds__(DIRECT ? 64 * kFastMaxWaves : 64 * kFastMaxWaves / 
         }
     };
     // X rows of a window into LDS
-    auto issue_direct = [&](int win, float *buf) {
+    auto issue_direct = [&](int win, SE *buf) {
         if constexpr (DIRECT) {
+            // lane l copies 16 bytes: row l / LPR, elements EPL * (l % LPR) ..
             const int xr0 = win * rpw;
             const int ninst = (rpw + RPI - 1) / RPI;
-            const int sub = lane / C4, c4 = lane % C4;
-            const int lane_x = sub * (int)ldx + t0 + 4 * c4;  // host checked: K * ldx < 2^31
+            const int sub = lane / LPR, ce = EPL * (lane % LPR);
+            const int lane_x = sub * (int)ldx + t0 + ce;  // host checked: K * ldx < 2^31
             for (int j = wave; j < ninst; j += nwaves) {
                 const int kb = xr0 + j * RPI;  // first row of this instruction (uniform)
                 if (kb + RPI <= K) {
                     lds_copy16(X + (int64_t)kb * ldx + lane_x, buf + j * RPI * TN);
                 } else {
                     const int k = min(kb + sub, K - 1);  // rows past K: never selected
-                    lds_copy16(X + (int64_t)k * ldx + t0 + 4 * c4, buf + j * RPI * TN);
+                    lds_copy16(X + (int64_t)k * ldx + t0 + ce, buf + j * RPI * TN);
                 }
             }
         } else {
@@ -150,12 +154,13 @@ __global__ __launch_bounds__(DIRECT ? 64 * kFastMaxWaves : 64 * kFastMaxWaves / 
             if (rr < rpw && k < K) xr[p] = load4<T>(X + (int64_t)k * ldx + tok, N - tok, xvec);
         }
     };
-    auto store_x = [&](const v4f (&xr)[XVMAX], float *buf) {
+    auto store_x = [&](const v4f (&xr)[XVMAX], SE *buf) {
 #pragma unroll
         for (int p = 0; p < XVMAX; ++p) {
             const int e = threadIdx.x + p * nthreads;
             const int rr = e / C4, c4 = e % C4;
-            if (rr < rpw) *reinterpret_cast<v4f *>(&buf[rr * TN + 4 * c4]) = xr[p];
+            if constexpr (!DIRECT)
+                if (rr < rpw) *reinterpret_cast<v4f *>(&buf[rr * TN + 4 * c4]) = xr[p];
         }
     };
 
@@ -179,7 +184,7 @@ __global__ __launch_bounds__(DIRECT ? 64 * kFastMaxWaves : 64 * kFastMaxWaves / 
 
     // window `win` from LDS buffer `cur` with weights `a` and index words `wv`;
     // window win+1 goes to `nxt`, `a_nxt`, `wv_nxt` meanwhile
-    auto step = [&](int win, float *cur, float *nxt, const float (&a)[QW], uint32_t wv,
+    auto step = [&](int win, SE *cur, SE *nxt, const float (&a)[QW], uint32_t wv,
                     float (&a_nxt)[QW], uint32_t &wv_nxt) {
         if constexpr (DIRECT) wait_all_memory();  // this wave's loads for `win` have landed
         __syncthreads();  // cur is complete; every wave is done with nxt
@@ -224,7 +229,7 @@ __global__ __launch_bounds__(DIRECT ? 64 * kFastMaxWaves : 64 * kFastMaxWaves / 
                     static_for<TPL>([&](auto pc) {
                         constexpr int p = decltype(pc)::value;
                         acc[q][p] = __builtin_amdgcn_mfma_f32_4x4x1f32(
-                            a[q], tok_part4<TPL>(b[s & 1][u], p), acc[q][p], CBSZ, s, 0);
+                            a[q], tok_part4<SE, TPL>(b[s & 1][u], p), acc[q][p], CBSZ, s, 0);
                     });
                 });
             });
@@ -270,8 +275,9 @@ __global__ __launch_bounds__(DIRECT ? 64 * kFastMaxWaves : 64 * kFastMaxWaves / 
 // the staged rows of the variant; 0 if none.  (The register-staged variant's
 // smaller budget decides whether the layout is taken at all.)
 int fast_window(const nmg_layout *L, int tpl, bool direct = false) {
+    const int es = direct ? (int)elem_size(L->dtype) : 4;
     for (int ksw = 16; ksw >= 4; ksw /= 2)
-        if (ksw % L->n == 0 && (ksw / L->n) * L->m <= fast_window_rows(tpl, direct)) return ksw;
+        if (ksw % L->n == 0 && (ksw / L->n) * L->m <= fast_window_rows(tpl, direct, es)) return ksw;
     return 0;
 }
 
@@ -304,9 +310,14 @@ nmg_status launch_fast_v(const nmg_layout *L, const void *values, const uint8_t 
         const int64_t slots = (int64_t)cus * kernel_occupancy(kern, 64 * w) * w;  // waves resident at once
         const int64_t rounds = (tiles * w + slots - 1) / slots;
         const double eff = (double)(tiles * w) / (double)(rounds * slots);
-        // best fill of whole rounds; on a tie the larger workgroup, whose
-        // staged X windows feed more rows
-        if (eff > best_eff - 1e-9) { best_eff = std::max(eff, best_eff); best_w = w; }
+        // best fill of whole rounds; on a tie the larger workgroup (its staged
+        // X windows feed more rows) -- unless the grid leaves CUs idle, where
+        // more, smaller workgroups spread the work wider
+        const bool tie = eff > best_eff - 1e-9 && eff < best_eff + 1e-9;
+        if (eff > best_eff + 1e-9 || (tie && tiles >= cus)) {
+            best_eff = std::max(eff, best_eff);
+            best_w = w;
+        }
     }
     const int row_tiles = (L->M + kFastRowsWave * best_w - 1) / (kFastRowsWave * best_w);
     const int tiles = row_tiles * tok_tiles;
@@ -324,10 +335,12 @@ nmg_status launch_fast_ut(const nmg_layout *L, const void *values, const uint8_t
                           const void *X, int64_t ldx, int N, void *Y, int64_t ldy,
                           hipStream_t stream) {
     const bool xvec = x_vectorisable(L, X, ldx);
-    const bool direct = std::is_same<T, float>::value && xvec && N % (64 * TPL) == 0;
+    // direct copies move 16 bytes per lane: 16-byte rows and whole token tiles
+    const bool direct = aligned(X, 16) && (ldx * (int64_t)sizeof(T)) % 16 == 0 &&
+                        N % (64 * TPL) == 0;
 #define NMG_FAST(KSW)                                                                           \
-    return direct ? launch_fast_v<T, U, KSW, TPL, std::is_same<T, float>::value>(                \
-                        L, values, indices, X, ldx, N, Y, ldy, xvec, stream)                    \
+    return direct ? launch_fast_v<T, U, KSW, TPL, true>(L, values, indices, X, ldx, N, Y, ldy,   \
+                                                        xvec, stream)                           \
                   : launch_fast_v<T, U, KSW, TPL, false>(L, values, indices, X, ldx, N, Y, ldy, \
                                                          xvec, stream)
     switch (fast_window(L, TPL, direct)) {
