@@ -89,11 +89,13 @@ typedef enum nmg_kernel {
                                     needs g % 4 == 0 and a window of 2..16
                                     k-slots (a power of two that n divides)
                                     whose chunks fit its staging buffer         */
-    NMG_KERNEL_MFMA_SCALAR = 4   /* the same product with scalar-loaded indices
-                                    and wider token tiles; additionally needs n a
-                                    power of two, C*n % 4 == 0, 4-byte aligned
-                                    indices and a window of 4..16 k-slots      */
+    NMG_KERNEL_MFMA_SCALAR = 4   /* the same product with the index words of a
+                                    window moved to scalar registers and wider
+                                    token tiles; additionally needs n a power of
+                                    two and a window of 4..16 k-slots          */
 } nmg_kernel;
+/* With n == m every column is kept and every index row is 0 .. m-1, so the
+ * matrix-core kernels treat the weight as one group whatever g is. */
 
 /* Checks 1 <= n <= m <= 255, g >= 1, M >= 1, K >= 1 (NMG_ERR_PARAM),
  * M % g == 0 and tail width >= n (NMG_ERR_SHAPE), a known dtype

@@ -91,6 +91,12 @@ nmg_status nmg_compress(const nmg_layout *L, const void *W, int64_t ldw, void *v
 
 nmg_kernel nmg_spmm_auto_kernel(const nmg_layout *L, int64_t N) {
     if (check_layout(L) != NMG_OK) return NMG_KERNEL_AUTO;
+    nmg_layout dense;
+    if (L->n == L->m && L->g != L->M) {  // as in nmg_spmm_with
+        dense = *L;
+        dense.g = L->M;
+        L = &dense;
+    }
     if (spmm_scalar_supported(L, nullptr, N)) return NMG_KERNEL_MFMA_SCALAR;
     return spmm_general_supported(L, N) ? NMG_KERNEL_MFMA_GENERAL : NMG_KERNEL_VALU;
 }
@@ -104,6 +110,14 @@ nmg_status nmg_spmm_with(const nmg_layout *L, nmg_kernel kernel, const void *val
     if (N < 1 || N > INT32_MAX || ldx < N || ldy < N) return NMG_ERR_PARAM;
     const size_t es = elem_size(L->dtype);
     if (!aligned(X, es) || !aligned(values, es) || !aligned(Y, es)) return NMG_ERR_ALIGN;
+    // n == m keeps every column, so every index row is 0 .. m-1: the whole
+    // weight is one group and the grouped kernels apply whatever g is
+    nmg_layout dense;
+    if (L->n == L->m && L->g != L->M) {
+        dense = *L;
+        dense.g = L->M;
+        L = &dense;
+    }
     const SpmmArgs a{L, values, indices, X, ldx, (int)N, Y, ldy, stream};
     const bool scalar_ok = spmm_scalar_supported(L, indices, ldx);
     if (kernel == NMG_KERNEL_AUTO) {

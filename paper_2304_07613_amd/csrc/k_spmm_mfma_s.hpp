@@ -111,9 +111,9 @@ __global__ __launch_bounds__(DIRECT ? 64 * kFastMaxWaves : 64 * kFastMaxWaves / 
         if (iw_u == u) iw_row = irow[u];
     auto load_idx = [&](int win, uint32_t &wv, bool guarded) {
         const uint8_t *p = iw_row + win * KSW + 4 * iw_j;
-        if (!guarded) {
+        if (!guarded && (reinterpret_cast<uintptr_t>(p) & 3) == 0) {
             wv = *reinterpret_cast<const uint32_t *>(p);
-        } else {
+        } else {  // the last window, or an index row not on a 4-byte boundary
             uint32_t x = 0;
 #pragma unroll
             for (int b = 0; b < 4; ++b)
@@ -284,8 +284,9 @@ int fast_window(const nmg_layout *L, int tpl, bool direct = false) {
 // `indices` may be NULL to ask about the layout alone.
 [[maybe_unused]] bool fast_supported(const nmg_layout *L, const uint8_t *indices, int64_t ldx) {
     const int64_t ldv = (int64_t)L->C * L->n;
-    return mfma_unit(L) != 0 && ldv % 4 == 0 && (!indices || aligned(indices, 4)) &&
-           (L->n & (L->n - 1)) == 0 && (int64_t)L->M * ldv < ((int64_t)1 << 31) &&
+    (void)indices;
+    return mfma_unit(L) != 0 && (L->n & (L->n - 1)) == 0 &&
+           (int64_t)L->M * ldv < ((int64_t)1 << 31) &&
            (int64_t)L->K * ldx < ((int64_t)1 << 31) && fast_window(L, 1) != 0;
 }
 

@@ -70,9 +70,12 @@ def test_calls_reject_bad_arguments_before_launch(lib):
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 32) == nmg.KERNELS["valu"]
     assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 1, 4, 8, nmg.F32) == nmg.OK
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_scalar"]
-    # C * n = 77 is not a multiple of 4: the general matrix-core kernel
-    assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 1, 10, 8, nmg.F32) == nmg.OK
-    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_general"]
+    # n = 3 is not a power of two: the general matrix-core kernel declines too
+    assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 3, 8, 8, nmg.F32) == nmg.OK
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["valu"]
+    # n = m (dense) with g = 1: one group, so the matrix cores take it
+    assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 4, 4, 1, nmg.F32) == nmg.OK
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_scalar"]
 
 
 def test_status_strings(lib):
