@@ -5,14 +5,13 @@
 
 namespace {
 
-// The fast matrix-core kernel, for layouts whose index rows are 4-byte
-// aligned (C*n % 4 == 0) and whose windows hold a multiple of 4 k-slots.
-// Differences from k_spmm_mfma: a wave owns 16 rows (4 quads) and 64*TPL
-// tokens; the workgroup has a runtime number of waves (4..8) so that the
-// tile count fits the GPU in whole rounds; the index bytes of a window are
-// fetched with scalar loads, so every gathered-row offset is computed on the
-// scalar unit (no lane-to-scalar moves); one LDS read of TPL tokens per lane
-// feeds TPL*U/4 matrix instructions.
+// The fast matrix-core kernel, for layouts with n a power of two and windows
+// of 4, 8 or 16 k-slots.  Differences from k_spmm_mfma: a wave owns 16 rows
+// (4 quads) and 64*TPL tokens; the workgroup has a runtime number of waves so
+// that the tile count fits the GPU in whole rounds; the index words of a
+// window are loaded by distinct lanes and moved to scalar registers once per
+// window, so every gathered-row offset is computed on the scalar unit; one LDS
+// read of TPL tokens per lane feeds TPL*U/4 matrix instructions.
 constexpr int kFastRowsWave = 16;                  // 4 quads
 constexpr int kFastMaxWaves = 16;
 // Staging buffers: 64 KB each when X is copied straight to LDS in its own
