@@ -89,10 +89,16 @@ typedef enum nmg_kernel {
                                     needs g % 4 == 0 and a window of 2..16
                                     k-slots (a power of two that n divides)
                                     whose chunks fit its staging buffer         */
-    NMG_KERNEL_MFMA_SCALAR = 4   /* the same product with the index words of a
+    NMG_KERNEL_MFMA_SCALAR = 4,  /* the same product with the index words of a
                                     window moved to scalar registers and wider
                                     token tiles; additionally needs n a power of
                                     two and a window of 4..16 k-slots          */
+    NMG_KERNEL_MFMA_F16 = 5      /* binary16 layouts on the binary16 matrix
+                                    cores, 4 k-slots per instruction (binary32
+                                    accumulation); needs g % 4 == 0, n a power
+                                    of two, a window of 4..32 k-slots whose
+                                    chunks fit 128 staged X rows, X and ldx on
+                                    16-byte boundaries and N % 8 == 0         */
 } nmg_kernel;
 /* With n == m every column is kept and every index row is 0 .. m-1, so the
  * matrix-core kernels treat the weight as one group whatever g is. */
@@ -135,7 +141,7 @@ nmg_status nmg_spmm_with(const nmg_layout *layout, nmg_kernel kernel,
                          int64_t ldy, hipStream_t stream);
 
 /* The kernel family NMG_KERNEL_AUTO picks for this layout and N, assuming
- * 4-byte aligned indices and ldx = N (never NMG_KERNEL_AUTO or
+ * 16-byte aligned X, 4-byte aligned indices and ldx = N (never
  * NMG_KERNEL_MFMA; NMG_KERNEL_AUTO only for an invalid layout). */
 nmg_kernel nmg_spmm_auto_kernel(const nmg_layout *layout, int64_t N);
 

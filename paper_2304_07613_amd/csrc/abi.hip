@@ -97,6 +97,7 @@ nmg_kernel nmg_spmm_auto_kernel(const nmg_layout *L, int64_t N) {
         dense.g = L->M;
         L = &dense;
     }
+    if (spmm_half_supported(L, nullptr, N, N)) return NMG_KERNEL_MFMA_F16;
     if (spmm_scalar_supported(L, nullptr, N)) return NMG_KERNEL_MFMA_SCALAR;
     return spmm_general_supported(L, N) ? NMG_KERNEL_MFMA_GENERAL : NMG_KERNEL_VALU;
 }
@@ -119,15 +120,19 @@ nmg_status nmg_spmm_with(const nmg_layout *L, nmg_kernel kernel, const void *val
         L = &dense;
     }
     const SpmmArgs a{L, values, indices, X, ldx, (int)N, Y, ldy, stream};
+    const bool half_ok = spmm_half_supported(L, X, ldx, N);
     const bool scalar_ok = spmm_scalar_supported(L, indices, ldx);
     if (kernel == NMG_KERNEL_AUTO) {
-        kernel = scalar_ok                        ? NMG_KERNEL_MFMA_SCALAR
+        kernel = half_ok                          ? NMG_KERNEL_MFMA_F16
+                 : scalar_ok                      ? NMG_KERNEL_MFMA_SCALAR
                  : spmm_general_supported(L, N) ? NMG_KERNEL_MFMA_GENERAL
                                                   : NMG_KERNEL_VALU;
     } else if (kernel == NMG_KERNEL_MFMA) {
-        kernel = scalar_ok ? NMG_KERNEL_MFMA_SCALAR : NMG_KERNEL_MFMA_GENERAL;
+        kernel = half_ok ? NMG_KERNEL_MFMA_F16 : scalar_ok ? NMG_KERNEL_MFMA_SCALAR : NMG_KERNEL_MFMA_GENERAL;
     }
     switch (kernel) {
+        case NMG_KERNEL_MFMA_F16:
+            return half_ok ? spmm_half(a) : NMG_ERR_UNSUPPORTED;
         case NMG_KERNEL_MFMA_SCALAR:
             return scalar_ok ? spmm_scalar(a) : NMG_ERR_UNSUPPORTED;
         case NMG_KERNEL_MFMA_GENERAL:

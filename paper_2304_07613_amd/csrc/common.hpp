@@ -91,6 +91,9 @@ nmg_status spmm_scalar_f32_u8(const SpmmArgs &a);
 nmg_status spmm_scalar_f32_u4(const SpmmArgs &a);
 nmg_status spmm_scalar_f16(const SpmmArgs &a);
 
+bool spmm_half_supported(const nmg_layout *L, const void *X, int64_t ldx, int64_t N);
+nmg_status spmm_half(const SpmmArgs &a);
+
 }  // namespace nmg_internal
 
 namespace {

@@ -1,0 +1,281 @@
+// k_spmm_mfma_h.hip -- the product Y = W_s X for binary16 layouts on the
+// binary16 matrix cores (v_mfma_f32_4x4x4_16b_f16, binary32 accumulation).
+//
+// Paper: STen (arXiv 2304.07613), Section 5.1 (the sparse x dense product of
+// the grouped n:m layout); the kernel itself is this library's design.
+//
+// The binary32 kernels multiply one gathered X row (one k-slot) per matrix
+// instruction.  The binary16 instruction contracts over 4 k-slots at once, so
+// each lane needs, for each of its tokens, the 4 gathered X values of 4
+// consecutive k-slots side by side.  X is staged in LDS row-major as in the
+// other kernels; a lane reads 4 tokens of each of the 4 gathered rows (one
+// 8-byte LDS read per row) and transposes the 4 x 4 block in registers, which
+// gives the B operands of its 4 tokens.  The A operand (4 rows x 4 k-slots of
+// weights) is broadcast from one block to all 16 blocks of the instruction, so
+// one instruction covers 4 rows x 64 tokens x 4 k-slots.
+#include "common.hpp"
+
+namespace {
+
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+
+constexpr int kHalfRowsWave = 16;        // 4 quads of 4 rows
+constexpr int kHalfTokens = 256;         // tokens per wave and workgroup (4 per lane)
+constexpr int kHalfMaxWaves = 12;        // 128 KB of LDS: one workgroup per CU
+constexpr int kHalfStageBytes = 65536;   // per staging buffer
+constexpr int kHalfWindowRows = kHalfStageBytes / (kHalfTokens * 2);  // 128 X rows
+
+template <int U, int KSW>
+__global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
+    const _Float16 *__restrict__ values, const uint8_t *__restrict__ indices,
+    const _Float16 *__restrict__ X, int64_t ldx, _Float16 *__restrict__ Y, int64_t ldy, int M,
+    int K, int N, int log2n, int m, int g, int C, int row_tiles, int tiles, bool avec, bool yvec) {
+    static_assert(KSW % 4 == 0 && U % 4 == 0 && U <= kHalfRowsWave, "k-groups of 4 slots");
+    constexpr int QW = kHalfRowsWave / 4;   // quads per wave
+    constexpr int UNITS = kHalfRowsWave / U;
+    constexpr int QPU = U / 4;              // quads per unit
+    constexpr int KG = KSW / 4;             // k-groups per window
+    constexpr int CBSZ = ilog2(KG);         // broadcast group of KG blocks
+    constexpr int IW = KSW / 4;             // index words per unit and window
+    constexpr int LPR = kHalfTokens / 8;    // lanes per staged row (16 bytes each)
+    constexpr int RPI = 64 / LPR;           // rows per copy instruction
+    static_assert(UNITS * IW <= 64, "one index word per lane");
+    __shared__ _Float16 xs0[kHalfStageBytes / 2];
+    __shared__ _Float16 xs1[kHalfStageBytes / 2];
+
+    const int nwaves = blockDim.x >> 6;
+    const int tile = xcd_tile(blockIdx.x, tiles);
+    const int rt = tile % row_tiles, tt = tile / row_tiles;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int r0 = rt * (kHalfRowsWave * nwaves) + wave * kHalfRowsWave;
+    const int t0 = tt * kHalfTokens;
+    const int n = 1 << log2n;
+    const int ldv = C * n;                  // host checked: M * ldv < 2^31
+    const int cpw = KSW >> log2n;           // chunks per window
+    const int rpw = cpw * m;                // X rows per window (<= kHalfWindowRows)
+    const int nwin = (C + cpw - 1) / cpw;
+    const bool ragged = nwin * KSW > ldv;   // the last window runs past the k-slots
+
+    // index row of each unit (rows past M read the last group; never stored)
+    const uint8_t *irow[UNITS];
+#pragma unroll
+    for (int u = 0; u < UNITS; ++u) irow[u] = indices + (int64_t)(min(r0 + u * U, M - 1) / g) * ldv;
+
+    // A operands: lane 4b+i holds row r0+4q+i, k-slots 4(b % KG) .. 4(b % KG)+3
+    // of the window (blocks beyond KG repeat the first KG, as the broadcast
+    // groups of CBSZ expect)
+    const int a_slot = 4 * ((lane >> 2) & (KG - 1));
+    int aoff[QW];
+#pragma unroll
+    for (int q = 0; q < QW; ++q) aoff[q] = min(r0 + 4 * q + (lane & 3), M - 1) * ldv + a_slot;
+    auto load_a = [&](int win, h4 (&a)[QW], bool guarded) {
+        const _Float16 *vb = values + win * KSW;
+#pragma unroll
+        for (int q = 0; q < QW; ++q) {
+            if (avec && !guarded) {
+                a[q] = *reinterpret_cast<const h4 *>(vb + aoff[q]);
+            } else {
+                h4 v;
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    v[k] = win * KSW + a_slot + k < ldv ? vb[aoff[q] + k] : (_Float16)0.f;
+                a[q] = v;
+            }
+        }
+    };
+    // index words of the window: lane u*IW + j loads word j of unit u
+    const int iw_u = min(lane / IW, UNITS - 1), iw_j = lane % IW;
+    const uint8_t *iw_row = irow[0];
+#pragma unroll
+    for (int u = 1; u < UNITS; ++u)
+        if (iw_u == u) iw_row = irow[u];
+    auto load_idx = [&](int win, uint32_t &wv, bool guarded) {
+        const uint8_t *p = iw_row + win * KSW + 4 * iw_j;
+        if (!guarded && (reinterpret_cast<uintptr_t>(p) & 3) == 0) {
+            wv = *reinterpret_cast<const uint32_t *>(p);
+        } else {  // the last window, or an index row not on a 4-byte boundary
+            uint32_t x = 0;
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+                if (win * KSW + 4 * iw_j + b < ldv) x |= (uint32_t)p[b] << (8 * b);
+            wv = x;
+        }
+    };
+    // X rows of a window into LDS: lane l copies 16 bytes (8 tokens) of row
+    // l / LPR; tokens past N (a ragged last token tile) re-read the row's last
+    // 8 tokens (host checked: N % 8 == 0), rows past K the last row -- both
+    // are staged but never used for a stored output
+    const int copy_sub = lane / LPR;
+    const int copy_tok = min(t0 + 8 * (lane % LPR), N - 8);
+    auto issue_copies = [&](int win, _Float16 *buf) {
+        const int ninst = (rpw + RPI - 1) / RPI;
+        for (int j = wave; j < ninst; j += nwaves) {
+            const int k = min(win * rpw + j * RPI + copy_sub, K - 1);
+            lds_copy16(X + (int64_t)k * ldx + copy_tok, buf + j * RPI * kHalfTokens);  // K * ldx < 2^31
+        }
+    };
+
+    v4f acc[QW][4];
+#pragma unroll
+    for (int q = 0; q < QW; ++q)
+#pragma unroll
+        for (int p = 0; p < 4; ++p) acc[q][p] = v4f{0.f, 0.f, 0.f, 0.f};
+
+    h4 a0[QW], a1[QW];          // weights of even / odd windows
+    uint32_t w0 = 0, w1 = 0;    // index words of even / odd windows (one per lane)
+    issue_copies(0, xs0);
+    load_a(0, a0, ragged && nwin == 1);
+    load_idx(0, w0, ragged && nwin == 1);
+
+    auto step = [&](int win, _Float16 *cur, _Float16 *nxt, const h4 (&a)[QW], uint32_t wv,
+                    h4 (&a_nxt)[QW], uint32_t &wv_nxt) {
+        wait_all_memory();  // this wave's copies and loads for `win` have landed
+        __syncthreads();    // cur is complete; every wave is done with nxt
+        uint32_t w[UNITS][IW];
+#pragma unroll
+        for (int u = 0; u < UNITS; ++u)
+#pragma unroll
+            for (int j = 0; j < IW; ++j) w[u][j] = __builtin_amdgcn_readlane(wv, u * IW + j);
+        if (win + 1 < nwin) {
+            const bool last_guarded = ragged && win + 2 == nwin;
+            issue_copies(win + 1, nxt);
+            load_a(win + 1, a_nxt, last_guarded);
+            load_idx(win + 1, wv_nxt, last_guarded);
+        }
+
+        const h4 *cv = reinterpret_cast<const h4 *>(cur);
+        // steps t = kg * UNITS + u: the 4 gathered rows (4 tokens each) of
+        // k-group kg of unit u, read one step ahead of their use
+        h4 r[2][4];
+        auto read_step = [&](auto tc, h4 (&dst)[4]) {
+            constexpr int kg = decltype(tc)::value / UNITS, u = decltype(tc)::value % UNITS;
+            static_for<4>([&](auto ic) {
+                constexpr int s = 4 * kg + decltype(ic)::value;
+                // scalar: byte s of the unit's index words, clamped into the chunk
+                const uint32_t o = min((w[u][s / 4] >> (8 * (s % 4))) & 0xffu, (uint32_t)(m - 1));
+                const uint32_t row = (uint32_t)((s >> log2n) * m) + o;
+                dst[decltype(ic)::value] = cv[row * 64 + lane];  // uniform row address
+            });
+        };
+        read_step(std::integral_constant<int, 0>{}, r[0]);
+        static_for<KG * UNITS>([&](auto tc) {
+            constexpr int t = decltype(tc)::value;
+            constexpr int kg = t / UNITS, u = t % UNITS;
+            if constexpr (t + 1 < KG * UNITS) read_step(std::integral_constant<int, t + 1>{}, r[(t + 1) & 1]);
+            // keep the reads of step t+1 ahead of the work of step t
+            __builtin_amdgcn_sched_barrier(0);
+            const h4 (&x)[4] = r[t & 1];
+            static_for<4>([&](auto pc) {
+                constexpr int p = decltype(pc)::value;
+                // B operand of token p: the 4 k-slots of the group side by side
+                const h4 b = {x[0][p], x[1][p], x[2][p], x[3][p]};
+                static_for<QPU>([&](auto qc) {
+                    constexpr int q = u * QPU + decltype(qc)::value;
+                    acc[q][p] = __builtin_amdgcn_mfma_f32_4x4x4f16(a[q], b, acc[q][p], CBSZ, kg, 0);
+                });
+            });
+        });
+    };
+    for (int win = 0; win < nwin; win += 2) {
+        step(win, xs0, xs1, a0, w0, a1, w1);
+        if (win + 1 < nwin) step(win + 1, xs1, xs0, a1, w1, a0, w0);
+    }
+
+    // output register i of (quad q, token p) at lane l is Y[r0 + 4q + i][t0 + 4l + p];
+    // binary32 -> binary16 rounds to nearest even
+    const int tok = t0 + 4 * lane;
+#pragma unroll
+    for (int q = 0; q < QW; ++q)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int row = r0 + 4 * q + i;
+            if (row >= M) continue;
+            _Float16 *y = Y + (int64_t)row * ldy + tok;
+            if (yvec && tok + 3 < N) {
+                const h4 v = {(_Float16)acc[q][0][i], (_Float16)acc[q][1][i], (_Float16)acc[q][2][i],
+                              (_Float16)acc[q][3][i]};
+                __builtin_nontemporal_store(v, reinterpret_cast<h4 *>(y));
+                continue;
+            }
+#pragma unroll
+            for (int p = 0; p < 4; ++p)
+                if (tok + p < N) __builtin_nontemporal_store((_Float16)acc[q][p][i], y + p);
+        }
+}
+
+// Largest window of 32, 16, 8 or 4 k-slots that n divides and whose chunks fit
+// the staging buffer; 0 if none.
+int half_window(const nmg_layout *L) {
+    for (int ksw = 32; ksw >= 4; ksw /= 2)
+        if (ksw % L->n == 0 && (ksw / L->n) * L->m <= kHalfWindowRows) return ksw;
+    return 0;
+}
+
+template <int U, int KSW>
+nmg_status launch_half(const SpmmArgs &a) {
+    const nmg_layout *L = a.L;
+    const void *kern = reinterpret_cast<const void *>(&k_spmm_mfma_h<U, KSW>);
+    // waves per workgroup: the count whose tiles fill whole rounds of the GPU best
+    const int cus = device_cus();
+    const int tok_tiles = (a.N + kHalfTokens - 1) / kHalfTokens;
+    int best_w = 4;
+    double best_eff = -1.0;
+    for (int w = 4; w <= kHalfMaxWaves; ++w) {
+        const int64_t tiles = (int64_t)((L->M + kHalfRowsWave * w - 1) / (kHalfRowsWave * w)) * tok_tiles;
+        const int64_t slots = (int64_t)cus * kernel_occupancy(kern, 64 * w) * w;
+        const int64_t rounds = (tiles * w + slots - 1) / slots;
+        const double eff = (double)(tiles * w) / (double)(rounds * slots);
+        const bool tie = eff > best_eff - 1e-9 && eff < best_eff + 1e-9;
+        if (eff > best_eff + 1e-9 || (tie && tiles >= cus)) {
+            best_eff = std::max(eff, best_eff);
+            best_w = w;
+        }
+    }
+    const int row_tiles = (L->M + kHalfRowsWave * best_w - 1) / (kHalfRowsWave * best_w);
+    const int tiles = row_tiles * tok_tiles;
+    const int64_t ldv = (int64_t)L->C * L->n;
+    const bool avec = aligned(a.values, 8) && ldv % 4 == 0;
+    const bool yvec = aligned(a.Y, 8) && a.ldy % 4 == 0;
+    int log2n = 0;
+    while ((1 << log2n) < L->n) ++log2n;
+    hipLaunchKernelGGL((k_spmm_mfma_h<U, KSW>), dim3(tiles), dim3(64 * best_w), 0, a.stream,
+                       (const _Float16 *)a.values, a.indices, (const _Float16 *)a.X, a.ldx,
+                       (_Float16 *)a.Y, a.ldy, L->M, L->K, a.N, log2n, L->m, L->g, L->C, row_tiles,
+                       tiles, avec, yvec);
+    return launched();
+}
+
+template <int U>
+nmg_status launch_half_u(const SpmmArgs &a) {
+    switch (half_window(a.L)) {
+        case 32: return launch_half<U, 32>(a);
+        case 16: return launch_half<U, 16>(a);
+        case 8: return launch_half<U, 8>(a);
+        case 4: return launch_half<U, 4>(a);
+        default: return NMG_ERR_UNSUPPORTED;
+    }
+}
+
+}  // namespace
+
+// The binary16 matrix-core kernel takes binary16 layouts whose groups are
+// whole quads (g % 4 == 0) with n a power of two and a window that fits its
+// staging buffer, and X that can be copied to LDS 16 bytes at a time: rows on
+// 16-byte boundaries (X and ldx) and N a multiple of 8.  Index and values
+// offsets must fit 31 bits.  `X` may be NULL to ask about the layout alone.
+bool nmg_internal::spmm_half_supported(const nmg_layout *L, const void *X, int64_t ldx, int64_t N) {
+    const int64_t ldv = (int64_t)L->C * L->n;
+    return L->dtype == NMG_F16 && mfma_unit(L) != 0 && (L->n & (L->n - 1)) == 0 &&
+           half_window(L) != 0 && (X == nullptr || aligned(X, 16)) && ldx % 8 == 0 && N % 8 == 0 &&
+           (int64_t)L->M * ldv < ((int64_t)1 << 31) && (int64_t)L->K * ldx < ((int64_t)1 << 31);
+}
+
+nmg_status nmg_internal::spmm_half(const SpmmArgs &a) {
+    switch (mfma_unit(a.L) >= 16 ? 16 : mfma_unit(a.L)) {
+        case 16: return launch_half_u<16>(a);
+        case 8: return launch_half_u<8>(a);
+        case 4: return launch_half_u<4>(a);
+        default: return NMG_ERR_UNSUPPORTED;
+    }
+}

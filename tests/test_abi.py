@@ -64,7 +64,7 @@ def test_calls_reject_bad_arguments_before_launch(lib):
     assert lib.nmg_compress(ctypes.byref(bad), p, 64, p, p, s) == nmg.ERR_PARAM
     # g % 4 != 0: the matrix-core kernel declines, the vector kernel is the choice
     assert lib.nmg_layout_init(ctypes.byref(L), 64, 64, 1, 4, 2, nmg.F32) == nmg.OK
-    for fam in ("mfma", "mfma_general", "mfma_scalar"):
+    for fam in ("mfma", "mfma_general", "mfma_scalar", "mfma_f16"):
         assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS[fam], p, p, p, 32, 32, p, 32,
                                  s) == nmg.ERR_UNSUPPORTED
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 32) == nmg.KERNELS["valu"]
@@ -76,6 +76,20 @@ def test_calls_reject_bad_arguments_before_launch(lib):
     # n = m (dense) with g = 1: one group, so the matrix cores take it
     assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 4, 4, 1, nmg.F32) == nmg.OK
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_scalar"]
+    # binary16: the binary16 matrix cores when X can be staged 16 bytes at a
+    # time (N % 8 == 0), else the binary32 matrix-core kernel on widened X
+    assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 2, 8, 8, nmg.F16) == nmg.OK
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_f16"]
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4100) == nmg.KERNELS["mfma_scalar"]
+    assert lib.nmg_layout_init(ctypes.byref(L), 768, 3072, 1, 10, 16, nmg.F16) == nmg.OK
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_f16"]
+    # a window of 4 k-slots at 1:255 needs 1020 staged rows: declined
+    assert lib.nmg_layout_init(ctypes.byref(L), 64, 510, 1, 255, 8, nmg.F16) == nmg.OK
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) != nmg.KERNELS["mfma_f16"]
+    assert lib.nmg_layout_init(ctypes.byref(L), 64, 64, 1, 4, 2, nmg.F16) == nmg.OK
+    assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS["mfma_f16"], p, p, p, 32, 32, p, 32,
+                             s) == nmg.ERR_UNSUPPORTED
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["valu"]
 
 
 def test_status_strings(lib):

@@ -81,7 +81,7 @@ def spmm_full(nmg, v, idx, L, X, rv, ridx, kernel, tag=""):
 
 
 # every kernel family; the matrix-core ones decline layouts they cannot take
-KERNELS = ["auto", "valu", "mfma_general", "mfma_scalar"]
+KERNELS = ["auto", "valu", "mfma_general", "mfma_scalar", "mfma_f16"]
 
 
 def kernels_for(nmg, L, N):
@@ -106,6 +106,15 @@ SMALL = [
     (768, 64, 40, 2, 4, 768, torch.float32),    # g = M
     (96, 48, 300, 2, 4, 12, torch.float16),     # g = 12 (unit of 4 rows)
     (512, 128, 260, 4, 8, 8, torch.float32),    # n = 4
+    # binary16 matrix cores (N % 8 == 0): ragged row and token tiles, one
+    # ragged window with unaligned value rows (C*n = 18)
+    (264, 72, 264, 2, 8, 8, torch.float16),
+    (512, 200, 520, 1, 4, 8, torch.float16),    # two windows, the last one ragged
+    (384, 768, 1024, 2, 8, 16, torch.float16),  # units of 16 rows, 6 windows
+    (192, 100, 136, 1, 10, 4, torch.float16),   # 1:10, windows of 8 k-slots, units of 4
+    (96, 48, 304, 2, 4, 12, torch.float16),     # g = 12
+    (64, 40, 8, 4, 4, 1, torch.float16),        # dense control, N = 8
+    (128, 84, 40, 1, 20, 32, torch.float16),    # 1:20, windows of 4 k-slots, tail 4
 ]
 
 
