@@ -43,7 +43,7 @@ FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense binary32 matrix peak
 FP32_VALU_PEAK_TFLOPS = 78.6    # binary32 vector FMA without packed math (2 FLOP/lane/clk)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "spmm_bert-ffn-up_traffic.txt")
 KERNEL_SYMBOL = {"mfma_scalar": "k_spmm_mfma_s", "mfma_general": "k_spmm_mfma",
-                 "valu": "k_spmm_valu"}
+                 "mfma_f16": "k_spmm_mfma_h", "valu": "k_spmm_valu"}
 
 
 def parse():
@@ -51,7 +51,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--kernel", choices=("auto", "mfma", "valu", "mfma_general", "mfma_scalar"),
+    ap.add_argument("--kernel", choices=("auto", "mfma", "valu", "mfma_general", "mfma_scalar",
+                                         "mfma_f16"),
                     default="auto")
     ap.add_argument("--workload", type=int, choices=(1, 2, 3), default=2)
     ap.add_argument("--sweep", action="store_true")
@@ -67,14 +68,27 @@ def parse():
     return ap.parse_args()
 
 
-def source_digest() -> str:
+# The sources that make the profiled kernels (the headline product and the
+# converter): the stored traffic figure holds while these are unchanged.
+TRAFFIC_SOURCES = ("common.hpp", "k_spmm_mfma_s.hpp", "k_spmm_mfma_s_f32_u8.hip",
+                   "k_elementwise.hip")
+
+
+def traffic_digest() -> str:
+    """Digest of the profiled kernels' sources (names and contents) and the header."""
+    import hashlib
     from paper_2304_07613_amd import build
-    return build.source_digest()
+    h = hashlib.sha256()
+    for p in [os.path.join(build.CSRC, f) for f in TRAFFIC_SOURCES] + [build.HEADER]:
+        h.update(os.path.relpath(p, ROOT).encode())
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def stored_traffic(digest: str):
     """HBM bytes per spmm launch from the committed rocprofv3 counter summary,
-    if it was taken on the current kernel source; else None."""
+    if it was taken on the current sources of the profiled kernels; else None."""
     try:
         with open(TRAFFIC_FILE) as f:
             text = f.read()
@@ -190,7 +204,7 @@ def family_times(ctx, L, sets, kernel, reps=20):
     the timed region): the evidence behind the automatic choice."""
     torch, nmg = ctx.torch, ctx.nmg
     out = {}
-    for fam in ("mfma_scalar", "mfma_general", "valu"):
+    for fam in ("mfma_f16", "mfma_scalar", "mfma_general", "valu"):
         try:
             for r in range(3):
                 W, X, v, idx, Y = sets[r % len(sets)]
@@ -295,7 +309,7 @@ def headline(ctx, args):
     res = time_layer(ctx, args, args.workload, 0, lin, args.kernel)
     rec = layer_record(lin, res)
     if args.workload == 2:
-        rec["roofline"]["traffic"] = stored_traffic(source_digest())
+        rec["roofline"]["traffic"] = stored_traffic(traffic_digest())
     out = {
         "metric": METRIC if args.workload == 2 else "nmg_spmm useful GFLOP/s",
         "value": round(lin.useful_flop / (res["ms_step"] * 1e-3) / 1e9, 1),

@@ -153,8 +153,11 @@ nmg_status nmg_densify(const nmg_layout *layout, const void *values,
 
 /* Elementwise glue between the layers of a linear stack (not in the paper's
  * format; BERT's encoder block).  `count` elements, contiguous, same dtype.
- *   nmg_gelu: out = 0.5 x (1 + erf(x / sqrt 2)), computed in binary32 as
- *             0.5 x erfc(-x / sqrt 2) (no cancellation for negative x).
+ *   nmg_gelu: out = 0.5 x (1 + erf(x / sqrt 2)).  binary16: looked up in a
+ *             table of every binary16 input, built from a binary64 evaluation
+ *             rounded to nearest even (NaN and -inf give NaN, +inf gives
+ *             +inf).  binary32: evaluated in binary32 as 0.5 x erfc(-x / sqrt 2)
+ *             (no cancellation for negative x).
  *   nmg_add : out = a + b, computed in binary32 (exactly rounded for
  *             binary16 operands).
  * In-place use (out == in / out == a) is allowed. */

@@ -2,14 +2,15 @@
 
 Every translation unit under csrc/ is compiled to an object in parallel, then
 the objects are linked into one shared library; the link is checked for
-undefined kernel launch stubs.
+undefined kernel launch stubs.  csrc/gen_gelu_table.py writes the binary16
+GELU table into the build folder first.
 """
 from __future__ import annotations
 
 import glob
-import hashlib
 import os
 import subprocess
+import sys
 import tempfile
 from concurrent.futures import ThreadPoolExecutor
 
@@ -32,19 +33,12 @@ def sources() -> list:
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
+GENERATORS = [os.path.join(CSRC, "gen_gelu_table.py")]
+
+
 def inputs() -> list:
     """Every file the library is built from."""
-    return sorted(sources() + glob.glob(os.path.join(CSRC, "*.hpp")) + [HEADER])
-
-
-def source_digest() -> str:
-    """Digest of every build input (names and contents)."""
-    h = hashlib.sha256()
-    for p in inputs():
-        h.update(os.path.relpath(p, ROOT).encode())
-        with open(p, "rb") as f:
-            h.update(f.read())
-    return h.hexdigest()[:16]
+    return sorted(sources() + glob.glob(os.path.join(CSRC, "*.hpp")) + [HEADER] + GENERATORS)
 
 
 def _clean(text: str) -> str:
@@ -58,6 +52,12 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
     jobs = jobs or min(16, os.cpu_count() or 4)
     inc = ["-I", os.path.join(ROOT, "include")]
     with tempfile.TemporaryDirectory(prefix="nmg_build_") as tmpdir:
+        # generated sources (the binary16 GELU table) go to the build folder
+        gen = subprocess.run([sys.executable, GENERATORS[0], os.path.join(tmpdir, "gelu_f16_table.inc")],
+                             capture_output=True, text=True)
+        if gen.returncode != 0:
+            raise RuntimeError(f"gen_gelu_table.py failed:\n{gen.stdout}{gen.stderr}")
+        inc += ["-I", tmpdir]
         def compile_one(src):
             obj = os.path.join(tmpdir, os.path.basename(src) + ".o")
             res = subprocess.run([hipcc, *HIPCC_FLAGS, *inc, "-c", "-o", obj, src],

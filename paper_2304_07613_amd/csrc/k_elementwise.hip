@@ -1,12 +1,15 @@
-// k_elementwise.hip -- dense -> n:m:g (Section 5.2), n:m:g -> dense, and the
-// elementwise glue of the linear stack.
+// k_elementwise.hip -- dense -> n:m:g (Section 5.2) and n:m:g -> dense.
 //
-//   k_compress  one thread per column of a chunk-block: binary32 group score
-//               down the g rows (coalesced across lanes), rank by counting
-//               inside the chunk through LDS, then a coalesced copy of the
-//               kept weights.  HBM-bound.
+//   k_compress_chunk  one thread per (group, chunk) for chunks of at most 32
+//               columns: the group scores of the chunk in registers (vector
+//               loads when the chunk starts on 16 bytes), ranked in
+//               registers; W is read once, every access coalesced across the
+//               wave.  HBM-bound.
+//   k_compress  one thread per column of a chunk-block (wide chunks, or few
+//               (group, chunk) pairs): binary32 group score down the g rows,
+//               rank by counting inside the chunk through LDS, then a
+//               coalesced copy of the kept weights.
 //   k_densify   one thread per output element.
-//   k_gelu, k_add
 #include "common.hpp"
 
 namespace {
@@ -181,22 +184,6 @@ __global__ __launch_bounds__(kBlock) void k_densify(
 
 // ------------------------------------------------------------- elementwise
 
-template <typename T>
-__global__ __launch_bounds__(kBlock) void k_gelu(const T *in, T *out, int64_t count) {
-    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (i >= count) return;
-    const float x = (float)in[i];
-    // 1 + erf(z) written as erfc(-z): no cancellation for negative x
-    out[i] = (T)(0.5f * x * erfcf(-x * 0.70710678118654752f));
-}
-
-template <typename T>
-__global__ __launch_bounds__(kBlock) void k_add(const T *a, const T *b, T *out, int64_t count) {
-    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (i >= count) return;
-    out[i] = (T)((float)a[i] + (float)b[i]);
-}
-
 }  // namespace
 
 namespace nmg_internal {
@@ -249,32 +236,6 @@ nmg_status launch_densify(const nmg_layout *L, const void *values, const uint8_t
         hipLaunchKernelGGL((k_densify<_Float16>), grid, dim3(kBlock), 0, stream,
                            (const _Float16 *)values, indices, (_Float16 *)W_out, ldw, L->K, L->n,
                            L->m, L->g, L->C);
-    return launched();
-}
-
-nmg_status launch_gelu(nmg_dtype dtype, const void *in, void *out, int64_t count,
-                       hipStream_t stream) {
-    const int64_t blocks = (count + kBlock - 1) / kBlock;
-    if (blocks > INT32_MAX) return NMG_ERR_PARAM;
-    if (dtype == NMG_F32)
-        hipLaunchKernelGGL((k_gelu<float>), dim3((unsigned)blocks), dim3(kBlock), 0, stream,
-                           (const float *)in, (float *)out, count);
-    else
-        hipLaunchKernelGGL((k_gelu<_Float16>), dim3((unsigned)blocks), dim3(kBlock), 0, stream,
-                           (const _Float16 *)in, (_Float16 *)out, count);
-    return launched();
-}
-
-nmg_status launch_add(nmg_dtype dtype, const void *a, const void *b, void *out, int64_t count,
-                      hipStream_t stream) {
-    const int64_t blocks = (count + kBlock - 1) / kBlock;
-    if (blocks > INT32_MAX) return NMG_ERR_PARAM;
-    if (dtype == NMG_F32)
-        hipLaunchKernelGGL((k_add<float>), dim3((unsigned)blocks), dim3(kBlock), 0, stream,
-                           (const float *)a, (const float *)b, (float *)out, count);
-    else
-        hipLaunchKernelGGL((k_add<_Float16>), dim3((unsigned)blocks), dim3(kBlock), 0, stream,
-                           (const _Float16 *)a, (const _Float16 *)b, (_Float16 *)out, count);
     return launched();
 }
 
