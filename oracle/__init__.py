@@ -68,11 +68,12 @@ def _load():
     i64, i32, vp = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p
     lib.oracle_compress.argtypes = [i32, i64, i64, i32, i32, i32, vp, i64, vp, vp]
     lib.oracle_densify.argtypes = [i32, i64, i64, i32, i32, i32, vp, vp, vp, i64, vp]
+    lib.oracle_repack.argtypes = [i32, i64, i64, i32, i32, i32, vp, i64, vp, vp]
     lib.oracle_spmm.argtypes = [i32, i64, i64, i32, i32, i32, vp, vp, vp, i64, i64,
                                 vp, vp, i32]
     lib.oracle_spmm_points.argtypes = [i32, i64, i64, i32, i32, i32, vp, vp, vp, i64,
                                        i64, i64, vp, vp, vp, vp]
-    for f in (lib.oracle_compress, lib.oracle_densify, lib.oracle_spmm,
+    for f in (lib.oracle_compress, lib.oracle_densify, lib.oracle_repack, lib.oracle_spmm,
               lib.oracle_spmm_points):
         f.restype = i32
     lib.oracle_half_to_float.argtypes = [ctypes.c_uint16]
@@ -120,6 +121,20 @@ def compress(W: np.ndarray, n: int, m: int, g: int):
     if st:
         raise OracleError(st, "compress")
     return values, indices
+
+
+def repack(W: np.ndarray, indices: np.ndarray, n: int, m: int, g: int) -> np.ndarray:
+    """Fixed-mask repack (Section 5.3, a sparsifier keeping the existing
+    format): W's entries at the positions `indices` selects, as values."""
+    W = np.ascontiguousarray(W)
+    indices = np.ascontiguousarray(indices, dtype=np.uint8)
+    dt = _dtype_code(W)
+    M, K = W.shape
+    values = np.empty((M, n_chunks(K, m) * n), dtype=W.dtype)
+    st = _load().oracle_repack(dt, M, K, n, m, g, _ptr(W), K, _ptr(indices), _ptr(values))
+    if st:
+        raise OracleError(st, "repack")
+    return values
 
 
 def densify(values: np.ndarray, indices: np.ndarray, K: int, n: int, m: int, g: int):

@@ -230,6 +230,33 @@ int oracle_compress(int dtype, int64_t M, int64_t K, int n, int m, int g,
     return ORC_OK;
 }
 
+/* ------------------------------------------------------------------ repack */
+
+/* The fixed-mask path after a weight update (Section 5.3: a sparsifier that
+ * keeps the tensor's existing format; the STen converters re-pack new dense
+ * values into the pattern already chosen).  The indices are given; values get
+ * W's entries at the kept positions:
+ *     values[r][c*n+s] = W[r][c*m + indices[r/g][c*n+s]]   (a bit copy). */
+int oracle_repack(int dtype, int64_t M, int64_t K, int n, int m, int g,
+                  const void *W, int64_t ldw, const uint8_t *indices, void *values)
+{
+    int st = check_layout(dtype, M, K, n, m, g);
+    if (st != ORC_OK)
+        return st;
+    if (ldw < K)
+        return ORC_EPARAM;
+    st = check_indices(M, K, n, m, g, indices);
+    if (st != ORC_OK)
+        return st;
+    int64_t C = n_chunks(K, m), ldv = C * n;
+    for (int64_t r = 0; r < M; ++r)
+        for (int64_t c = 0; c < C; ++c)
+            for (int s = 0; s < n; ++s)
+                copy_elem(dtype, values, ldv, r, c * n + s, W, ldw, r,
+                          c * m + indices[(r / g) * ldv + c * n + s]);
+    return ORC_OK;
+}
+
 /* ----------------------------------------------------------------- densify */
 
 /* W_out (M x K, leading dimension ldw) gets the kept values at their original

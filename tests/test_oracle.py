@@ -402,3 +402,48 @@ def test_linear_stack_layer_dense_control():
     diff = np.abs(got.astype(np.float64) - ref.astype(np.float64))
     ulp = np.spacing(np.abs(ref).astype(np.float16)).astype(np.float64)
     assert np.all(diff <= ulp)
+
+
+# --------------------------------------------------------- fixed-mask repack
+
+def test_repack_hand_example():
+    gold = load_golden("repack_2_4_2.json")
+    W2 = np.array(gold["W2"], np.float32)
+    idx = np.array(gold["indices"], np.uint8)
+    got = oracle.repack(W2, idx, gold["n"], gold["m"], gold["g"])
+    want = np.array(gold["values"], np.float32)
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32))  # -0 kept
+
+
+@pytest.mark.parametrize("n,m,g,M,K,dtype", [
+    (2, 4, 4, 16, 22, np.float32), (1, 10, 8, 16, 33, np.float16), (3, 8, 2, 6, 21, np.float32),
+    (4, 4, 1, 5, 12, np.float16), (1, 1, 3, 9, 7, np.float32)])
+def test_repack_agrees_with_compress_and_densify(n, m, g, M, K, dtype):
+    """Against two independently pinned parts of the oracle: re-packing W into
+    its own pattern gives the converter's values, and any other weight packed
+    into that pattern densifies to that weight masked by the pattern."""
+    rng = np.random.default_rng(M * K + n)
+    W = rng.standard_normal((M, K)).astype(dtype)
+    values, indices = oracle.compress(W, n, m, g)
+    assert np.array_equal(oracle.repack(W, indices, n, m, g).view(np.uint8), values.view(np.uint8))
+    W2 = rng.standard_normal((M, K)).astype(dtype)
+    W2[0, 0] = -0.0
+    v2 = oracle.repack(W2, indices, n, m, g)
+    dense, mask = oracle.densify(v2, indices, K, n, m, g)
+    want = np.where(mask, W2, np.zeros_like(W2))
+    assert np.array_equal(dense.view(np.uint8), want.view(np.uint8))
+    assert mask.sum() == M * n * n_chunks_of(K, m)
+
+
+def n_chunks_of(K, m):
+    return -(-K // m)
+
+
+def test_repack_rejects_invalid_indices():
+    W = np.zeros((4, 10), np.float32)
+    values, indices = oracle.compress(W, 1, 4, 2)
+    bad = indices.copy()
+    bad[1, 2] = 3  # tail chunk of width 2
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.repack(W, bad, 1, 4, 2)
+    assert e.value.status == 3
