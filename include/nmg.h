@@ -121,6 +121,15 @@ int64_t nmg_indices_numel(const nmg_layout *layout);
 nmg_status nmg_compress(const nmg_layout *layout, const void *W, int64_t ldw,
                         void *values, uint8_t *indices, hipStream_t stream);
 
+/* Fixed-mask repack (Section 5.3: the sparsifier that keeps a tensor's
+ * existing format, used when updated weights are sparsified again): values
+ * get W's entries at the positions `indices` selects, a bit copy; indices are
+ * only read.  W: M x K, leading dimension ldw >= K, element-aligned.  Indices
+ * must hold n strictly ascending in-chunk offsets per (group, chunk); other
+ * contents give unspecified values, but no read leaves W's row. */
+nmg_status nmg_repack(const nmg_layout *layout, const void *W, int64_t ldw,
+                      const uint8_t *indices, void *values, hipStream_t stream);
+
 /* Y = W_s * X (Section 5.1).  X: K x N, leading dimension ldx; Y: M x N,
  * leading dimension ldy; N >= 1, ldx >= N, ldy >= N; values, X and Y aligned
  * to their element size (NMG_ERR_ALIGN).  X rows that start on 16-byte (fp32)
@@ -139,6 +148,26 @@ nmg_status nmg_spmm_with(const nmg_layout *layout, nmg_kernel kernel,
                          const void *values, const uint8_t *indices,
                          const void *X, int64_t ldx, int64_t N, void *Y,
                          int64_t ldy, hipStream_t stream);
+
+/* What happens to the product before it is stored (the glue of a BERT
+ * encoder block folded into the product; not part of the paper's format).
+ * P is W_s * X rounded to the element type, exactly what nmg_spmm writes. */
+typedef enum nmg_epilogue {
+    NMG_EPILOGUE_NONE = 0,   /* Y = P                                      */
+    NMG_EPILOGUE_GELU = 1,   /* Y = GELU(P), as nmg_gelu computes it        */
+    NMG_EPILOGUE_ADD = 2     /* Y = P + R, as nmg_add computes it           */
+} nmg_epilogue;
+
+/* nmg_spmm_with followed by an epilogue; the result equals nmg_spmm_with
+ * followed by nmg_gelu or nmg_add bit for bit.  NMG_KERNEL_MFMA_F16 applies
+ * the epilogue in the product kernel (no second pass over Y); the other
+ * families run the elementwise kernel on Y afterwards.  R (ADD only; ignored
+ * otherwise, may be NULL) is M x N with leading dimension ldr >= N, the
+ * layout's element type, element-aligned, and must not overlap Y. */
+nmg_status nmg_spmm_epilogue(const nmg_layout *layout, nmg_kernel kernel, nmg_epilogue epilogue,
+                             const void *values, const uint8_t *indices, const void *X,
+                             int64_t ldx, int64_t N, const void *R, int64_t ldr, void *Y,
+                             int64_t ldy, hipStream_t stream);
 
 /* The kernel family NMG_KERNEL_AUTO picks for this layout and N, assuming
  * 16-byte aligned X, 4-byte aligned indices and ldx = N (never

@@ -89,10 +89,21 @@ nmg_status nmg_compress(const nmg_layout *L, const void *W, int64_t ldw, void *v
     return launch_compress(L, W, ldw, values, indices, stream);
 }
 
+nmg_status nmg_repack(const nmg_layout *L, const void *W, int64_t ldw, const uint8_t *indices,
+                      void *values, hipStream_t stream) {
+    nmg_status st = check_layout(L);
+    if (st != NMG_OK) return st;
+    if (!W || !indices || !values) return NMG_ERR_NULL;
+    if (ldw < L->K) return NMG_ERR_PARAM;
+    const size_t es = elem_size(L->dtype);
+    if (!aligned(W, es) || !aligned(values, es)) return NMG_ERR_ALIGN;
+    return launch_repack(L, W, ldw, indices, values, stream);
+}
+
 nmg_kernel nmg_spmm_auto_kernel(const nmg_layout *L, int64_t N) {
     if (check_layout(L) != NMG_OK) return NMG_KERNEL_AUTO;
     nmg_layout dense;
-    if (L->n == L->m && L->g != L->M) {  // as in nmg_spmm_with
+    if (L->n == L->m && L->g != L->M) {  // as in nmg_spmm_epilogue
         dense = *L;
         dense.g = L->M;
         L = &dense;
@@ -105,12 +116,32 @@ nmg_kernel nmg_spmm_auto_kernel(const nmg_layout *L, int64_t N) {
 nmg_status nmg_spmm_with(const nmg_layout *L, nmg_kernel kernel, const void *values,
                          const uint8_t *indices, const void *X, int64_t ldx, int64_t N, void *Y,
                          int64_t ldy, hipStream_t stream) {
+    return nmg_spmm_epilogue(L, kernel, NMG_EPILOGUE_NONE, values, indices, X, ldx, N, nullptr, 0,
+                             Y, ldy, stream);
+}
+
+nmg_status nmg_spmm_epilogue(const nmg_layout *L, nmg_kernel kernel, nmg_epilogue epi,
+                             const void *values, const uint8_t *indices, const void *X,
+                             int64_t ldx, int64_t N, const void *R, int64_t ldr, void *Y,
+                             int64_t ldy, hipStream_t stream) {
     nmg_status st = check_layout(L);
     if (st != NMG_OK) return st;
     if (!values || !indices || !X || !Y) return NMG_ERR_NULL;
     if (N < 1 || N > INT32_MAX || ldx < N || ldy < N) return NMG_ERR_PARAM;
     const size_t es = elem_size(L->dtype);
     if (!aligned(X, es) || !aligned(values, es) || !aligned(Y, es)) return NMG_ERR_ALIGN;
+    if (epi != NMG_EPILOGUE_NONE && epi != NMG_EPILOGUE_GELU && epi != NMG_EPILOGUE_ADD)
+        return NMG_ERR_PARAM;
+    if (epi == NMG_EPILOGUE_ADD) {
+        if (!R) return NMG_ERR_NULL;
+        if (ldr < N) return NMG_ERR_PARAM;
+        if (!aligned(R, es)) return NMG_ERR_ALIGN;
+        // R must not overlap Y (the unfused families write Y before reading R)
+        const uintptr_t r0 = reinterpret_cast<uintptr_t>(R), y0 = reinterpret_cast<uintptr_t>(Y);
+        const uintptr_t r1 = r0 + (uintptr_t)(((int64_t)(L->M - 1) * ldr + N) * (int64_t)es);
+        const uintptr_t y1 = y0 + (uintptr_t)(((int64_t)(L->M - 1) * ldy + N) * (int64_t)es);
+        if (r0 < y1 && y0 < r1) return NMG_ERR_PARAM;
+    }
     // n == m keeps every column, so every index row is 0 .. m-1: the whole
     // weight is one group and the grouped kernels apply whatever g is
     nmg_layout dense;
@@ -119,7 +150,7 @@ nmg_status nmg_spmm_with(const nmg_layout *L, nmg_kernel kernel, const void *val
         dense.g = L->M;
         L = &dense;
     }
-    const SpmmArgs a{L, values, indices, X, ldx, (int)N, Y, ldy, stream};
+    SpmmArgs a{L, values, indices, X, ldx, (int)N, Y, ldy, stream};
     const bool half_ok = spmm_half_supported(L, X, ldx, N);
     const bool scalar_ok = spmm_scalar_supported(L, indices, ldx);
     if (kernel == NMG_KERNEL_AUTO) {
@@ -132,17 +163,38 @@ nmg_status nmg_spmm_with(const nmg_layout *L, nmg_kernel kernel, const void *val
     }
     switch (kernel) {
         case NMG_KERNEL_MFMA_F16:
-            return half_ok ? spmm_half(a) : NMG_ERR_UNSUPPORTED;
+            if (!half_ok) return NMG_ERR_UNSUPPORTED;
+            a.epi = epi;  // applied in the product kernel
+            a.R = R;
+            a.ldr = ldr;
+            return spmm_half(a);
         case NMG_KERNEL_MFMA_SCALAR:
-            return scalar_ok ? spmm_scalar(a) : NMG_ERR_UNSUPPORTED;
+            if (!scalar_ok) return NMG_ERR_UNSUPPORTED;
+            st = spmm_scalar(a);
+            break;
         case NMG_KERNEL_MFMA_GENERAL:
             if (!spmm_general_supported(L, N)) return NMG_ERR_UNSUPPORTED;
-            return L->dtype == NMG_F32 ? spmm_general_f32(a) : spmm_general_f16(a);
+            st = L->dtype == NMG_F32 ? spmm_general_f32(a) : spmm_general_f16(a);
+            break;
         case NMG_KERNEL_VALU:
-            return spmm_valu(a);
+            st = spmm_valu(a);
+            break;
         default:
             return NMG_ERR_PARAM;
     }
+    if (st != NMG_OK || epi == NMG_EPILOGUE_NONE) return st;
+    // the epilogue as a second pass over Y (row by row when rows are not contiguous)
+    const bool flat = ldy == N && (epi != NMG_EPILOGUE_ADD || ldr == N);
+    const int64_t rows = flat ? 1 : L->M, count = flat ? (int64_t)L->M * N : N;
+    for (int64_t r = 0; r < rows; ++r) {
+        char *y = static_cast<char *>(Y) + (size_t)(r * ldy) * es;
+        st = epi == NMG_EPILOGUE_GELU
+                 ? launch_gelu(L->dtype, y, y, count, stream)
+                 : launch_add(L->dtype, y, static_cast<const char *>(R) + (size_t)(r * ldr) * es, y,
+                              count, stream);
+        if (st != NMG_OK) return st;
+    }
+    return NMG_OK;
 }
 
 nmg_status nmg_spmm(const nmg_layout *L, const void *values, const uint8_t *indices,

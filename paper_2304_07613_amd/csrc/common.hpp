@@ -67,10 +67,15 @@ struct SpmmArgs {
     void *Y;
     int64_t ldy;
     hipStream_t stream;
+    nmg_epilogue epi = NMG_EPILOGUE_NONE;  // applied by kernels that fuse it
+    const void *R = nullptr;               // residual (NMG_EPILOGUE_ADD)
+    int64_t ldr = 0;
 };
 
 nmg_status launch_compress(const nmg_layout *L, const void *W, int64_t ldw, void *values,
                            uint8_t *indices, hipStream_t stream);
+nmg_status launch_repack(const nmg_layout *L, const void *W, int64_t ldw, const uint8_t *indices,
+                         void *values, hipStream_t stream);
 nmg_status launch_densify(const nmg_layout *L, const void *values, const uint8_t *indices,
                           void *W_out, int64_t ldw, hipStream_t stream);
 nmg_status launch_gelu(nmg_dtype dtype, const void *in, void *out, int64_t count,

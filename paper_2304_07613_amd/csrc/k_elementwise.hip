@@ -10,6 +10,7 @@
 //               rank by counting inside the chunk through LDS, then a
 //               coalesced copy of the kept weights.
 //   k_densify   one thread per output element.
+//   k_repack    one thread per kept slot: values from W at given indices.
 #include "common.hpp"
 
 namespace {
@@ -182,7 +183,23 @@ __global__ __launch_bounds__(kBlock) void k_densify(
     reinterpret_cast<B *>(out)[r * ldw + k] = v;
 }
 
-// ------------------------------------------------------------- elementwise
+// Fixed-mask repack: one thread per kept slot of a row; the offset is clamped
+// into its chunk, so malformed indices never read outside the row.
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_repack(
+    const T *__restrict__ W, int64_t ldw, const uint8_t *__restrict__ indices,
+    T *__restrict__ values, int K, int n, int m, int g, int C) {
+    using B = typename Bits<T>::type;
+    const int64_t r = blockIdx.x;
+    const int64_t ldv = (int64_t)C * n;
+    const int j = blockIdx.y * kBlock + threadIdx.x;  // kept slot c * n + s
+    if (j >= ldv) return;
+    const int c = j / n;
+    const int w = min(m, K - c * m);
+    const int o = min((int)indices[(r / g) * ldv + j], w - 1);
+    reinterpret_cast<B *>(values)[r * ldv + j] =
+        reinterpret_cast<const B *>(W)[r * ldw + (int64_t)c * m + o];
+}
 
 }  // namespace
 
@@ -235,6 +252,20 @@ nmg_status launch_densify(const nmg_layout *L, const void *values, const uint8_t
     else
         hipLaunchKernelGGL((k_densify<_Float16>), grid, dim3(kBlock), 0, stream,
                            (const _Float16 *)values, indices, (_Float16 *)W_out, ldw, L->K, L->n,
+                           L->m, L->g, L->C);
+    return launched();
+}
+
+nmg_status launch_repack(const nmg_layout *L, const void *W, int64_t ldw, const uint8_t *indices,
+                         void *values, hipStream_t stream) {
+    const int64_t ldv = (int64_t)L->C * L->n;
+    dim3 grid(L->M, (unsigned)((ldv + kBlock - 1) / kBlock));
+    if (L->dtype == NMG_F32)
+        hipLaunchKernelGGL((k_repack<float>), grid, dim3(kBlock), 0, stream, (const float *)W, ldw,
+                           indices, (float *)values, L->K, L->n, L->m, L->g, L->C);
+    else
+        hipLaunchKernelGGL((k_repack<_Float16>), grid, dim3(kBlock), 0, stream,
+                           (const _Float16 *)W, ldw, indices, (_Float16 *)values, L->K, L->n,
                            L->m, L->g, L->C);
     return launched();
 }

@@ -13,11 +13,22 @@
 // gives the B operands of its 4 tokens.  The A operand (4 rows x 4 k-slots of
 // weights) is broadcast from one block to all 16 blocks of the instruction, so
 // one instruction covers 4 rows x 64 tokens x 4 k-slots.
+//
+// Epilogues (fused, so that Y is written once): GELU looks the rounded
+// product up in the binary16 GELU table, copied into the staging buffers once
+// the last window is done; ADD reads the residual beside the store.  Both
+// give exactly what the product followed by nmg_gelu or nmg_add gives.
 #include "common.hpp"
 
 namespace {
 
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+
+// GELU(x) for every binary16 x, indexed by the bits of x (the table nmg_gelu
+// uses, generated at build time)
+__device__ __attribute__((aligned(16))) const uint16_t g_gelu_f16[65536] = {
+#include "gelu_f16_table.inc"
+};
 
 constexpr int kHalfRowsWave = 16;        // 4 quads of 4 rows
 constexpr int kHalfTokens = 256;         // tokens per wave and workgroup (4 per lane)
@@ -25,11 +36,12 @@ constexpr int kHalfMaxWaves = 12;        // 128 KB of LDS: one workgroup per CU
 constexpr int kHalfStageBytes = 65536;   // per staging buffer
 constexpr int kHalfWindowRows = kHalfStageBytes / (kHalfTokens * 2);  // 128 X rows
 
-template <int U, int KSW>
+template <int U, int KSW, int EPI>
 __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
     const _Float16 *__restrict__ values, const uint8_t *__restrict__ indices,
-    const _Float16 *__restrict__ X, int64_t ldx, _Float16 *__restrict__ Y, int64_t ldy, int M,
-    int K, int N, int log2n, int m, int g, int C, int row_tiles, int tiles, bool avec, bool yvec) {
+    const _Float16 *__restrict__ X, int64_t ldx, _Float16 *__restrict__ Y, int64_t ldy,
+    const _Float16 *__restrict__ R, int64_t ldr, int M, int K, int N, int log2n, int m, int g,
+    int C, int row_tiles, int tiles, bool avec, bool yvec, bool rvec) {
     static_assert(KSW % 4 == 0 && U % 4 == 0 && U <= kHalfRowsWave, "k-groups of 4 slots");
     constexpr int QW = kHalfRowsWave / 4;   // quads per wave
     constexpr int UNITS = kHalfRowsWave / U;
@@ -182,8 +194,33 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
         if (win + 1 < nwin) step(win + 1, xs1, xs0, a1, w1, a0, w0);
     }
 
-    // output register i of (quad q, token p) at lane l is Y[r0 + 4q + i][t0 + 4l + p];
-    // binary32 -> binary16 rounds to nearest even
+    if constexpr (EPI == NMG_EPILOGUE_GELU) {
+        // the GELU table into the staging buffers: entries of non-negative
+        // inputs (sign bit clear) in xs0, of negative ones in xs1
+        __syncthreads();  // every wave is done with the last window
+        const uint4 *src = reinterpret_cast<const uint4 *>(g_gelu_f16);
+        constexpr int HALF4 = kHalfStageBytes / 16;
+        for (int i = threadIdx.x; i < 2 * HALF4; i += blockDim.x)
+            reinterpret_cast<uint4 *>(i < HALF4 ? xs0 : xs1)[i % HALF4] = src[i];
+        __syncthreads();
+    }
+    // the value stored for product v (binary32) and residual r
+    auto finish = [&](float v, _Float16 r) -> _Float16 {
+        const _Float16 h = (_Float16)v;  // round to nearest even, as nmg_spmm stores it
+        if constexpr (EPI == NMG_EPILOGUE_GELU) {
+            const uint16_t b = __builtin_bit_cast(uint16_t, h);
+            const uint16_t *tab = reinterpret_cast<const uint16_t *>((b & 0x8000u) ? xs1 : xs0);
+            (void)r;
+            return __builtin_bit_cast(_Float16, tab[b & 0x7fffu]);
+        } else if constexpr (EPI == NMG_EPILOGUE_ADD) {
+            return (_Float16)((float)h + (float)r);
+        } else {
+            (void)r;
+            return h;
+        }
+    };
+
+    // output register i of (quad q, token p) at lane l is Y[r0 + 4q + i][t0 + 4l + p]
     const int tok = t0 + 4 * lane;
 #pragma unroll
     for (int q = 0; q < QW; ++q)
@@ -192,15 +229,26 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
             const int row = r0 + 4 * q + i;
             if (row >= M) continue;
             _Float16 *y = Y + (int64_t)row * ldy + tok;
+            h4 rr = {(_Float16)0.f, (_Float16)0.f, (_Float16)0.f, (_Float16)0.f};
+            if constexpr (EPI == NMG_EPILOGUE_ADD) {
+                const _Float16 *rp = R + (int64_t)row * ldr + tok;
+                if (rvec && tok + 3 < N) {
+                    rr = *reinterpret_cast<const h4 *>(rp);
+                } else {
+#pragma unroll
+                    for (int p = 0; p < 4; ++p)
+                        if (tok + p < N) rr[p] = rp[p];
+                }
+            }
             if (yvec && tok + 3 < N) {
-                const h4 v = {(_Float16)acc[q][0][i], (_Float16)acc[q][1][i], (_Float16)acc[q][2][i],
-                              (_Float16)acc[q][3][i]};
+                const h4 v = {finish(acc[q][0][i], rr[0]), finish(acc[q][1][i], rr[1]),
+                              finish(acc[q][2][i], rr[2]), finish(acc[q][3][i], rr[3])};
                 __builtin_nontemporal_store(v, reinterpret_cast<h4 *>(y));
                 continue;
             }
 #pragma unroll
             for (int p = 0; p < 4; ++p)
-                if (tok + p < N) __builtin_nontemporal_store((_Float16)acc[q][p][i], y + p);
+                if (tok + p < N) __builtin_nontemporal_store(finish(acc[q][p][i], rr[p]), y + p);
         }
 }
 
@@ -212,10 +260,10 @@ int half_window(const nmg_layout *L) {
     return 0;
 }
 
-template <int U, int KSW>
+template <int U, int KSW, int EPI>
 nmg_status launch_half(const SpmmArgs &a) {
     const nmg_layout *L = a.L;
-    const void *kern = reinterpret_cast<const void *>(&k_spmm_mfma_h<U, KSW>);
+    const void *kern = reinterpret_cast<const void *>(&k_spmm_mfma_h<U, KSW, EPI>);
     // waves per workgroup: the count whose tiles fill whole rounds of the GPU best
     const int cus = device_cus();
     const int tok_tiles = (a.N + kHalfTokens - 1) / kHalfTokens;
@@ -237,22 +285,33 @@ nmg_status launch_half(const SpmmArgs &a) {
     const int64_t ldv = (int64_t)L->C * L->n;
     const bool avec = aligned(a.values, 8) && ldv % 4 == 0;
     const bool yvec = aligned(a.Y, 8) && a.ldy % 4 == 0;
+    const bool rvec = a.R && aligned(a.R, 8) && a.ldr % 4 == 0;
     int log2n = 0;
     while ((1 << log2n) < L->n) ++log2n;
-    hipLaunchKernelGGL((k_spmm_mfma_h<U, KSW>), dim3(tiles), dim3(64 * best_w), 0, a.stream,
+    hipLaunchKernelGGL((k_spmm_mfma_h<U, KSW, EPI>), dim3(tiles), dim3(64 * best_w), 0, a.stream,
                        (const _Float16 *)a.values, a.indices, (const _Float16 *)a.X, a.ldx,
-                       (_Float16 *)a.Y, a.ldy, L->M, L->K, a.N, log2n, L->m, L->g, L->C, row_tiles,
-                       tiles, avec, yvec);
+                       (_Float16 *)a.Y, a.ldy, (const _Float16 *)a.R, a.ldr, L->M, L->K, a.N,
+                       log2n, L->m, L->g, L->C, row_tiles, tiles, avec, yvec, rvec);
     return launched();
+}
+
+template <int U, int KSW>
+nmg_status launch_half_e(const SpmmArgs &a) {
+    switch (a.epi) {
+        case NMG_EPILOGUE_NONE: return launch_half<U, KSW, NMG_EPILOGUE_NONE>(a);
+        case NMG_EPILOGUE_GELU: return launch_half<U, KSW, NMG_EPILOGUE_GELU>(a);
+        case NMG_EPILOGUE_ADD: return launch_half<U, KSW, NMG_EPILOGUE_ADD>(a);
+        default: return NMG_ERR_PARAM;
+    }
 }
 
 template <int U>
 nmg_status launch_half_u(const SpmmArgs &a) {
     switch (half_window(a.L)) {
-        case 32: return launch_half<U, 32>(a);
-        case 16: return launch_half<U, 16>(a);
-        case 8: return launch_half<U, 8>(a);
-        case 4: return launch_half<U, 4>(a);
+        case 32: return launch_half_e<U, 32>(a);
+        case 16: return launch_half_e<U, 16>(a);
+        case 8: return launch_half_e<U, 8>(a);
+        case 4: return launch_half_e<U, 4>(a);
         default: return NMG_ERR_UNSUPPORTED;
     }
 }

@@ -24,6 +24,7 @@ F32, F16 = 0, 1
 _DTYPE_CODE = {torch.float32: F32, torch.float16: F16}
 KERNELS = {"auto": 0, "valu": 1, "mfma": 2, "mfma_general": 3, "mfma_scalar": 4, "mfma_f16": 5}
 _KERNEL_NAME = {v: k for k, v in KERNELS.items()}
+EPILOGUES = {"none": 0, "gelu": 1, "add": 2}
 
 OK, ERR_NULL, ERR_PARAM, ERR_SHAPE, ERR_DTYPE, ERR_ALIGN, ERR_LAUNCH, ERR_UNSUPPORTED = range(8)
 
@@ -66,8 +67,11 @@ def lib():
         "nmg_values_numel": ([lp], i64),
         "nmg_indices_numel": ([lp], i64),
         "nmg_compress": ([lp, vp, i64, vp, vp, vp], ctypes.c_int),
+        "nmg_repack": ([lp, vp, i64, vp, vp, vp], ctypes.c_int),
         "nmg_spmm": ([lp, vp, vp, vp, i64, i64, vp, i64, vp], ctypes.c_int),
         "nmg_spmm_with": ([lp, ctypes.c_int, vp, vp, vp, i64, i64, vp, i64, vp], ctypes.c_int),
+        "nmg_spmm_epilogue": ([lp, ctypes.c_int, ctypes.c_int, vp, vp, vp, i64, i64, vp, i64, vp,
+                               i64, vp], ctypes.c_int),
         "nmg_spmm_auto_kernel": ([lp, i64], ctypes.c_int),
         "nmg_densify": ([lp, vp, vp, vp, i64, vp], ctypes.c_int),
         "nmg_gelu": ([ctypes.c_int, vp, vp, i64, vp], ctypes.c_int),
@@ -172,6 +176,22 @@ def compress(W: torch.Tensor, n: int, m: int, g: int):
     return values, indices, layout
 
 
+def repack(W: torch.Tensor, indices: torch.Tensor, layout: Layout) -> torch.Tensor:
+    """Dense W (M x K, GPU) packed into the existing pattern `indices`
+    (the fixed-mask path after a weight update) -> values."""
+    _need_cuda(W, indices)
+    if W.dtype != layout.dtype or indices.dtype != torch.uint8:
+        raise TypeError("dtype mismatch")
+    if tuple(W.shape) != (layout.M, layout.K):
+        raise ValueError(f"W must be {layout.M} x {layout.K}")
+    if tuple(indices.shape) != layout.indices_shape or not indices.is_contiguous():
+        raise ValueError(f"indices must be contiguous {layout.indices_shape}")
+    values = torch.empty(layout.values_shape, dtype=W.dtype, device=W.device)
+    _check(lib().nmg_repack(ctypes.byref(layout.c), _ptr(W), _rows(W, "W"), _ptr(indices),
+                            _ptr(values), _stream(W)), "nmg_repack")
+    return values
+
+
 def spmm_into(layout: Layout, values, indices, X, Y, kernel: str = "auto"):
     """``nmg_spmm_with`` into a caller-allocated Y (M x N)."""
     _need_cuda(values, indices, X, Y)
@@ -192,6 +212,39 @@ def spmm(values, indices, X, layout: Layout, kernel: str = "auto"):
     """Y = W_s X for the packed weight (values, indices)."""
     Y = torch.empty((layout.M, X.shape[1]), dtype=X.dtype, device=X.device)
     spmm_into(layout, values, indices, X, Y, kernel)
+    return Y
+
+
+def spmm_epilogue(values, indices, X, layout: Layout, epilogue: str = "none", R=None,
+                  kernel: str = "auto", Y=None):
+    """Y = epilogue(W_s X): "none", "gelu" (GELU of the product) or "add"
+    (product + R), bit for bit what spmm followed by gelu or add gives."""
+    _need_cuda(values, indices, X)
+    if X.dtype != layout.dtype or values.dtype != layout.dtype:
+        raise TypeError("dtype mismatch")
+    if X.shape[0] != layout.K:
+        raise ValueError("X must be K x N")
+    if tuple(values.shape) != layout.values_shape or not values.is_contiguous():
+        raise ValueError(f"values must be contiguous {layout.values_shape}")
+    if tuple(indices.shape) != layout.indices_shape or not indices.is_contiguous():
+        raise ValueError(f"indices must be contiguous {layout.indices_shape}")
+    N = X.shape[1]
+    if Y is None:
+        Y = torch.empty((layout.M, N), dtype=X.dtype, device=X.device)
+    _need_cuda(Y)
+    if Y.dtype != layout.dtype or tuple(Y.shape) != (layout.M, N):
+        raise ValueError("Y must be M x N of the layout's dtype")
+    rp, ldr = ctypes.c_void_p(0), 0
+    if epilogue == "add":
+        if R is None:
+            raise ValueError("the add epilogue needs R")
+        _need_cuda(R)
+        if R.dtype != layout.dtype or tuple(R.shape) != (layout.M, N):
+            raise ValueError("R must be M x N of the layout's dtype")
+        rp, ldr = _ptr(R), _rows(R, "R")
+    _check(lib().nmg_spmm_epilogue(ctypes.byref(layout.c), KERNELS[kernel], EPILOGUES[epilogue],
+                                   _ptr(values), _ptr(indices), _ptr(X), _rows(X, "X"), N, rp,
+                                   ldr, _ptr(Y), _rows(Y, "Y"), _stream(X)), "nmg_spmm_epilogue")
     return Y
 
 

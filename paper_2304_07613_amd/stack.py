@@ -11,7 +11,9 @@ encoder block (without LayerNorm):
 
 Activations are features x tokens (768 x 4096), binary16 in memory, binary32
 inside every kernel.  Every step runs in libnmg's kernels; torch only holds
-the buffers.
+the buffers.  By default GELU and the residual sums are folded into the
+products (``nmg_spmm_epilogue``); with a trace every step runs on its own so
+that each intermediate can be checked, and both give the same bits.
 """
 from __future__ import annotations
 
@@ -58,21 +60,28 @@ class LinearStack:
         self.nmg.spmm_into(L, v, idx, x, out)
         return out
 
+    def fused(self, layer: StackLayer, name: str, x: torch.Tensor, epilogue: str, r=None):
+        v, idx, L = layer.packed[name]
+        return self.nmg.spmm_epilogue(v, idx, x, L, epilogue, r)
+
     def forward_layer(self, layer: StackLayer, x: torch.Tensor, trace: dict | None = None):
         nmg = self.nmg
         d = x.shape[0]
         qkv = self.linear(layer, "qkv", x)
         vpart = qkv[2 * d:3 * d]                 # rows of V: a contiguous view
+        if trace is None:                        # GELU and residuals fused into the products
+            h = self.fused(layer, "ao", vpart, "add", x)
+            gl = self.fused(layer, "up", h, "gelu")
+            return self.fused(layer, "down", gl, "add", h)
         a = self.linear(layer, "ao", vpart)
         h = nmg.add(x, a)
         u = self.linear(layer, "up", h)
         gl = nmg.gelu(u)
         dn = self.linear(layer, "down", gl)
         out = nmg.add(h, dn)
-        if trace is not None:
-            trace["linear"] = {"qkv": (x, qkv), "ao": (vpart, a), "up": (h, u), "down": (gl, dn)}
-            trace["gelu"] = (u, gl)
-            trace["add"] = [(x, a, h), (h, dn, out)]
+        trace["linear"] = {"qkv": (x, qkv), "ao": (vpart, a), "up": (h, u), "down": (gl, dn)}
+        trace["gelu"] = (u, gl)
+        trace["add"] = [(x, a, h), (h, dn, out)]
         return out
 
     def forward(self, x: torch.Tensor) -> torch.Tensor:

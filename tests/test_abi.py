@@ -57,6 +57,16 @@ def test_calls_reject_bad_arguments_before_launch(lib):
     assert lib.nmg_spmm(ctypes.byref(L), p, p, p, 32, 32, odd, 32, s) == nmg.ERR_ALIGN
     assert lib.nmg_spmm(ctypes.byref(L), None, p, p, 32, 32, p, 32, s) == nmg.ERR_NULL
     assert lib.nmg_densify(ctypes.byref(L), p, p, p, 60, s) == nmg.ERR_PARAM
+    assert lib.nmg_repack(ctypes.byref(L), p, 60, p, p, s) == nmg.ERR_PARAM    # ldw < K
+    assert lib.nmg_repack(ctypes.byref(L), p, 64, None, p, s) == nmg.ERR_NULL
+    assert lib.nmg_repack(ctypes.byref(L), odd, 64, p, p, s) == nmg.ERR_ALIGN
+    ep = lib.nmg_spmm_epilogue
+    big = ctypes.c_void_p(1 << 30)  # far from p: no overlap
+    assert ep(ctypes.byref(L), 0, 7, p, p, p, 32, 32, None, 0, p, 32, s) == nmg.ERR_PARAM  # epilogue
+    assert ep(ctypes.byref(L), 0, 2, p, p, p, 32, 32, None, 32, p, 32, s) == nmg.ERR_NULL  # no R
+    assert ep(ctypes.byref(L), 0, 2, p, p, p, 32, 32, big, 16, p, 32, s) == nmg.ERR_PARAM  # ldr < N
+    assert ep(ctypes.byref(L), 0, 2, p, p, p, 32, 32, odd, 32, p, 32, s) == nmg.ERR_ALIGN
+    assert ep(ctypes.byref(L), 0, 2, p, p, p, 32, 32, p, 32, p, 32, s) == nmg.ERR_PARAM   # R == Y
     assert lib.nmg_gelu(9, p, p, 10, s) == nmg.ERR_DTYPE
     assert lib.nmg_add(nmg.F16, p, None, p, 10, s) == nmg.ERR_NULL
     assert lib.nmg_gelu(nmg.F32, p, p, 0, s) == nmg.OK   # empty input: nothing to launch

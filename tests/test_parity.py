@@ -132,6 +132,91 @@ def test_small_shapes(nmg, M, K, N, n, m, g, dtype):
         spmm_full(nmg, v, idx, L, X, rv, ridx, kernel, "small")
 
 
+# ------------------------------------------------------ fixed-mask repack
+
+def random_patterns(rng, groups, K, n, m):
+    """Valid index rows drawn at random (not from the converter)."""
+    C = -(-K // m)
+    idx = np.empty((groups, C * n), np.uint8)
+    for G in range(groups):
+        for c in range(C):
+            w = min(m, K - c * m)
+            idx[G, c * n:(c + 1) * n] = np.sort(rng.choice(w, n, replace=False))
+    return idx
+
+
+@pytest.mark.parametrize("M,K,n,m,g,dtype", [
+    (64, 70, 2, 4, 8, torch.float32), (96, 300, 1, 10, 16, torch.float16),
+    (40, 35, 3, 8, 4, torch.float32), (3072, 768, 1, 4, 8, torch.float32),
+    (2304, 768, 2, 8, 8, torch.float16), (8, 255, 7, 255, 2, torch.float16)])
+def test_repack(nmg, M, K, n, m, g, dtype):
+    rng = np.random.default_rng(M + K)
+    W = synth.normal((M, K), 61 + M, 0.02, dtype)
+    idx = random_patterns(rng, M // g, K, n, m)
+    print(f"[repack] {M}x{K} {n}:{m}:{g} {dtype}", flush=True)
+    L = nmg.Layout(M, K, n, m, g, dtype)
+    v = nmg.repack(W.to(DEV), torch.from_numpy(idx).to(DEV), L)
+    torch.cuda.synchronize()
+    rv = oracle.repack(np_of(W), idx, n, m, g)
+    assert np.array_equal(bits(np_of(v)), bits(rv))
+    # a weight re-packed into its own pattern gives the converter's values
+    v2, idx2, L2 = nmg.compress(W.to(DEV), n, m, g)
+    assert torch.equal(nmg.repack(W.to(DEV), idx2, L2).view(torch.uint8), v2.view(torch.uint8))
+
+
+# --------------------------------------------------------- fused epilogues
+
+@pytest.mark.parametrize("M,K,N,n,m,g,dtype", [
+    (264, 72, 264, 2, 8, 8, torch.float16), (768, 768, 4096, 2, 8, 8, torch.float16),
+    (3072, 768, 512, 2, 8, 8, torch.float16), (96, 48, 77, 2, 4, 12, torch.float16),
+    (128, 100, 136, 1, 10, 4, torch.float32), (64, 40, 33, 3, 8, 2, torch.float32)])
+def test_spmm_epilogue_equals_composition(nmg, M, K, N, n, m, g, dtype):
+    """GELU / residual folded into the product give the bits of the product
+    followed by nmg_gelu / nmg_add, for every kernel family that takes the
+    layout; the pieces themselves are checked against the oracle elsewhere."""
+    W = synth.normal((M, K), 71 + M, 0.02, dtype).to(DEV)
+    X = synth.normal((K, N), 72 + N, 1.0, dtype).to(DEV)
+    R = synth.normal((M, N), 73 + N, 1.0, dtype).to(DEV)
+    v, idx, L = nmg.compress(W, n, m, g)
+    for kernel in KERNELS:
+        print(f"[epilogue] {M}x{K}x{N} {n}:{m}:{g} {dtype} kernel={kernel}", flush=True)
+        try:
+            P = nmg.spmm(v, idx, X, L, kernel)
+        except nmg.NmgError as e:
+            assert e.status == nmg.ERR_UNSUPPORTED and kernel not in ("auto", "valu")
+            continue
+        Yg = nmg.spmm_epilogue(v, idx, X, L, "gelu", kernel=kernel)
+        Ya = nmg.spmm_epilogue(v, idx, X, L, "add", R, kernel=kernel)
+        Yn = nmg.spmm_epilogue(v, idx, X, L, "none", kernel=kernel)
+        torch.cuda.synchronize()
+        assert torch.equal(Yn.view(torch.uint8), P.view(torch.uint8))
+        assert torch.equal(Yg.view(torch.uint8), nmg.gelu(P).view(torch.uint8)), kernel
+        assert torch.equal(Ya.view(torch.uint8), nmg.add(P, R).view(torch.uint8)), kernel
+    # strided Y and R (the second pass runs row by row on the unfused families)
+    Yb = torch.zeros((M, N + 8), dtype=dtype, device=DEV)
+    Rb = torch.zeros((M, N + 8), dtype=dtype, device=DEV)
+    Rb[:, :N] = R
+    Ys = nmg.spmm_epilogue(v, idx, X, L, "add", Rb[:, :N], Y=Yb[:, :N])
+    torch.cuda.synchronize()
+    assert torch.equal(Ys.view(torch.uint8), nmg.add(nmg.spmm(v, idx, X, L), R).view(torch.uint8))
+    assert (Yb[:, N:] == 0).all()
+
+
+def test_stack_fused_equals_stepwise(nmg):
+    """One BERT layer: the fused forward gives the bits of the step-by-step
+    forward whose every step the stack test checks against the oracle."""
+    from paper_2304_07613_amd.stack import LinearStack
+    stack = LinearStack.from_workload(4, nmg, n_layers=2, keep_dense=False)
+    x = synth.normal((synth.BERT_HIDDEN, synth.BERT_TOKENS), synth.seed_for(4, 0, "X"), 1.0,
+                     torch.float16).to(DEV)
+    for layer in stack.layers:
+        fused = stack.forward_layer(layer, x)
+        stepwise = stack.forward_layer(layer, x, trace={})
+        torch.cuda.synchronize()
+        assert torch.equal(fused.view(torch.uint8), stepwise.view(torch.uint8))
+        x = fused
+
+
 # ----------------------------------------------------------- edge cases
 
 def test_ties_signed_zeros_and_nan(nmg):
