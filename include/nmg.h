@@ -96,9 +96,10 @@ typedef enum nmg_kernel {
     NMG_KERNEL_MFMA_F16 = 5      /* binary16 layouts on the binary16 matrix
                                     cores, 4 k-slots per instruction (binary32
                                     accumulation); needs g % 4 == 0, n a power
-                                    of two, a window of 4..32 k-slots whose
-                                    chunks fit 128 staged X rows, X and ldx on
-                                    16-byte boundaries and N % 8 == 0         */
+                                    of two, the chunks of max(4, n) k-slots
+                                    within 512 staged X rows (m <= 128 for
+                                    n <= 4), X and ldx on 16-byte boundaries
+                                    and N % 8 == 0                            */
 } nmg_kernel;
 /* With n == m every column is kept and every index row is 0 .. m-1, so the
  * matrix-core kernels treat the weight as one group whatever g is. */

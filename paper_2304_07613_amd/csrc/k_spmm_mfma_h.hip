@@ -6,13 +6,16 @@
 //
 // The binary32 kernels multiply one gathered X row (one k-slot) per matrix
 // instruction.  The binary16 instruction contracts over 4 k-slots at once, so
-// each lane needs, for each of its tokens, the 4 gathered X values of 4
-// consecutive k-slots side by side.  X is staged in LDS row-major as in the
-// other kernels; a lane reads 4 tokens of each of the 4 gathered rows (one
-// 8-byte LDS read per row) and transposes the 4 x 4 block in registers, which
-// gives the B operands of its 4 tokens.  The A operand (4 rows x 4 k-slots of
-// weights) is broadcast from one block to all 16 blocks of the instruction, so
-// one instruction covers 4 rows x 64 tokens x 4 k-slots.
+// each lane needs, for its token, the 4 gathered X values of 4 consecutive
+// k-slots side by side.  X is staged in LDS row-major as in the other
+// kernels, and one transposing LDS read (ds_read_b64_tr_b16) delivers exactly
+// that: within each 16-lane group, lane i receives element i % 4 of the 8-byte
+// loads of lanes i/4, i/4 + 4, i/4 + 8 and i/4 + 12.  So the lanes 4k .. 4k+3
+// of a group load 16 consecutive tokens of the gathered row of slot k, and
+// every lane gets its own token's 4 slots, with no shuffles.  The A operand
+// (4 rows x 4 k-slots of weights) is broadcast from one block to all 16
+// blocks of the instruction, so one instruction covers 4 rows x 64 tokens x 4
+// k-slots.  A wave covers 64 * TPL tokens: lane l owns tokens l + 64p.
 //
 // Epilogues (fused, so that Y is written once): GELU looks the rounded
 // product up in the binary16 GELU table, copied into the staging buffers once
@@ -31,25 +34,39 @@ __device__ __attribute__((aligned(16))) const uint16_t g_gelu_f16[65536] = {
 };
 
 constexpr int kHalfRowsWave = 16;        // 4 quads of 4 rows
-constexpr int kHalfTokens = 256;         // tokens per wave and workgroup (4 per lane)
 constexpr int kHalfMaxWaves = 12;        // 128 KB of LDS: one workgroup per CU
 constexpr int kHalfStageBytes = 65536;   // per staging buffer
-constexpr int kHalfWindowRows = kHalfStageBytes / (kHalfTokens * 2);  // 128 X rows
+// staged X rows per window for 64 * TPL tokens per row
+__host__ __device__ constexpr int half_window_rows(int tpl) { return kHalfStageBytes / (128 * tpl); }
 
-template <int U, int KSW, int EPI>
+typedef short s4 __attribute__((ext_vector_type(4)));
+
+// The transposing LDS read of 8 bytes at `p` (an address in LDS).
+__device__ __forceinline__ h4 lds_read_tr(const _Float16 *p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    return __builtin_bit_cast(
+        h4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4 *)p));
+#else
+    (void)p;
+    return h4{};
+#endif
+}
+
+template <int U, int KSW, int TPL>
 __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
     const _Float16 *__restrict__ values, const uint8_t *__restrict__ indices,
     const _Float16 *__restrict__ X, int64_t ldx, _Float16 *__restrict__ Y, int64_t ldy,
     const _Float16 *__restrict__ R, int64_t ldr, int M, int K, int N, int log2n, int m, int g,
-    int C, int row_tiles, int tiles, bool avec, bool yvec, bool rvec) {
-    static_assert(KSW % 4 == 0 && U % 4 == 0 && U <= kHalfRowsWave, "k-groups of 4 slots");
+    int C, int row_tiles, int tiles, int epi, bool avec) {
+    static_assert(KSW % 4 == 0 && KSW <= 64 && U % 4 == 0 && U <= kHalfRowsWave, "k-groups of 4 slots");
     constexpr int QW = kHalfRowsWave / 4;   // quads per wave
     constexpr int UNITS = kHalfRowsWave / U;
     constexpr int QPU = U / 4;              // quads per unit
     constexpr int KG = KSW / 4;             // k-groups per window
     constexpr int CBSZ = ilog2(KG);         // broadcast group of KG blocks
     constexpr int IW = KSW / 4;             // index words per unit and window
-    constexpr int LPR = kHalfTokens / 8;    // lanes per staged row (16 bytes each)
+    constexpr int TN = 64 * TPL;            // tokens per wave and workgroup
+    constexpr int LPR = TN / 8;             // lanes per staged row (16 bytes each)
     constexpr int RPI = 64 / LPR;           // rows per copy instruction
     static_assert(UNITS * IW <= 64, "one index word per lane");
     __shared__ _Float16 xs0[kHalfStageBytes / 2];
@@ -61,11 +78,11 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int r0 = rt * (kHalfRowsWave * nwaves) + wave * kHalfRowsWave;
-    const int t0 = tt * kHalfTokens;
+    const int t0 = tt * TN;
     const int n = 1 << log2n;
     const int ldv = C * n;                  // host checked: M * ldv < 2^31
     const int cpw = KSW >> log2n;           // chunks per window
-    const int rpw = cpw * m;                // X rows per window (<= kHalfWindowRows)
+    const int rpw = cpw * m;                // X rows per window (<= half_window_rows(TPL))
     const int nwin = (C + cpw - 1) / cpw;
     const bool ragged = nwin * KSW > ldv;   // the last window runs past the k-slots
 
@@ -124,15 +141,22 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
         const int ninst = (rpw + RPI - 1) / RPI;
         for (int j = wave; j < ninst; j += nwaves) {
             const int k = min(win * rpw + j * RPI + copy_sub, K - 1);
-            lds_copy16(X + (int64_t)k * ldx + copy_tok, buf + j * RPI * kHalfTokens);  // K * ldx < 2^31
+            lds_copy16(X + (int64_t)k * ldx + copy_tok, buf + j * RPI * TN);  // K * ldx < 2^31
         }
     };
 
-    v4f acc[QW][4];
+    // transposing reads: lane l loads slot k_l = (l >> 2) & 3 of a k-group,
+    // 4 tokens at tr_tok = 16 (l >> 4) + 4 (l & 3) of each 64-token block
+    const int k_l = (lane >> 2) & 3;
+    const uint32_t tr_shift = 8 * k_l;                    // its byte of an index word
+    const uint32_t tr_chunk = (uint32_t)((k_l >> log2n) * m);  // its slot's chunk within the k-group
+    const uint32_t tr_tok = 16 * (lane >> 4) + 4 * (lane & 3);
+
+    v4f acc[QW][TPL];
 #pragma unroll
     for (int q = 0; q < QW; ++q)
 #pragma unroll
-        for (int p = 0; p < 4; ++p) acc[q][p] = v4f{0.f, 0.f, 0.f, 0.f};
+        for (int p = 0; p < TPL; ++p) acc[q][p] = v4f{0.f, 0.f, 0.f, 0.f};
 
     h4 a0[QW], a1[QW];          // weights of even / odd windows
     uint32_t w0 = 0, w1 = 0;    // index words of even / odd windows (one per lane)
@@ -156,18 +180,18 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
             load_idx(win + 1, wv_nxt, last_guarded);
         }
 
-        const h4 *cv = reinterpret_cast<const h4 *>(cur);
-        // steps t = kg * UNITS + u: the 4 gathered rows (4 tokens each) of
-        // k-group kg of unit u, read one step ahead of their use
-        h4 r[2][4];
-        auto read_step = [&](auto tc, h4 (&dst)[4]) {
+        // steps t = kg * UNITS + u: the B operands of k-group kg of unit u
+        // (one transposing read per 64-token block), read one step ahead
+        h4 r[2][TPL];
+        auto read_step = [&](auto tc, h4 (&dst)[TPL]) {
             constexpr int kg = decltype(tc)::value / UNITS, u = decltype(tc)::value % UNITS;
-            static_for<4>([&](auto ic) {
-                constexpr int s = 4 * kg + decltype(ic)::value;
-                // scalar: byte s of the unit's index words, clamped into the chunk
-                const uint32_t o = min((w[u][s / 4] >> (8 * (s % 4))) & 0xffu, (uint32_t)(m - 1));
-                const uint32_t row = (uint32_t)((s >> log2n) * m) + o;
-                dst[decltype(ic)::value] = cv[row * 64 + lane];  // uniform row address
+            // this lane's slot 4 kg + k_l: chunk base, then its offset (clamped into the chunk)
+            const uint32_t base = (uint32_t)(((4 * kg) >> log2n) * m) + tr_chunk;
+            const uint32_t o = min((w[u][kg] >> tr_shift) & 0xffu, (uint32_t)(m - 1));
+            const _Float16 *rp = cur + (base + o) * TN + tr_tok;
+            static_for<TPL>([&](auto pc) {
+                constexpr int p = decltype(pc)::value;
+                dst[p] = lds_read_tr(rp + 64 * p);
             });
         };
         read_step(std::integral_constant<int, 0>{}, r[0]);
@@ -177,14 +201,11 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
             if constexpr (t + 1 < KG * UNITS) read_step(std::integral_constant<int, t + 1>{}, r[(t + 1) & 1]);
             // keep the reads of step t+1 ahead of the work of step t
             __builtin_amdgcn_sched_barrier(0);
-            const h4 (&x)[4] = r[t & 1];
-            static_for<4>([&](auto pc) {
+            static_for<TPL>([&](auto pc) {
                 constexpr int p = decltype(pc)::value;
-                // B operand of token p: the 4 k-slots of the group side by side
-                const h4 b = {x[0][p], x[1][p], x[2][p], x[3][p]};
                 static_for<QPU>([&](auto qc) {
                     constexpr int q = u * QPU + decltype(qc)::value;
-                    acc[q][p] = __builtin_amdgcn_mfma_f32_4x4x4f16(a[q], b, acc[q][p], CBSZ, kg, 0);
+                    acc[q][p] = __builtin_amdgcn_mfma_f32_4x4x4f16(a[q], r[t & 1][p], acc[q][p], CBSZ, kg, 0);
                 });
             });
         });
@@ -194,7 +215,7 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
         if (win + 1 < nwin) step(win + 1, xs1, xs0, a1, w1, a0, w0);
     }
 
-    if constexpr (EPI == NMG_EPILOGUE_GELU) {
+    if (epi == NMG_EPILOGUE_GELU) {
         // the GELU table into the staging buffers: entries of non-negative
         // inputs (sign bit clear) in xs0, of negative ones in xs1
         __syncthreads();  // every wave is done with the last window
@@ -204,69 +225,62 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
             reinterpret_cast<uint4 *>(i < HALF4 ? xs0 : xs1)[i % HALF4] = src[i];
         __syncthreads();
     }
-    // the value stored for product v (binary32) and residual r
-    auto finish = [&](float v, _Float16 r) -> _Float16 {
-        const _Float16 h = (_Float16)v;  // round to nearest even, as nmg_spmm stores it
-        if constexpr (EPI == NMG_EPILOGUE_GELU) {
-            const uint16_t b = __builtin_bit_cast(uint16_t, h);
-            const uint16_t *tab = reinterpret_cast<const uint16_t *>((b & 0x8000u) ? xs1 : xs0);
-            (void)r;
-            return __builtin_bit_cast(_Float16, tab[b & 0x7fffu]);
-        } else if constexpr (EPI == NMG_EPILOGUE_ADD) {
-            return (_Float16)((float)h + (float)r);
-        } else {
-            (void)r;
-            return h;
-        }
-    };
-
-    // output register i of (quad q, token p) at lane l is Y[r0 + 4q + i][t0 + 4l + p]
-    const int tok = t0 + 4 * lane;
+    // output register i of (quad q, block p) at lane l is Y[r0 + 4q + i][t0 + 64p + l];
+    // each store instruction writes 64 consecutive tokens
+    auto store_all = [&](auto ec) {
+        constexpr int E = decltype(ec)::value;
 #pragma unroll
-    for (int q = 0; q < QW; ++q)
+        for (int q = 0; q < QW; ++q)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int row = r0 + 4 * q + i;
-            if (row >= M) continue;
-            _Float16 *y = Y + (int64_t)row * ldy + tok;
-            h4 rr = {(_Float16)0.f, (_Float16)0.f, (_Float16)0.f, (_Float16)0.f};
-            if constexpr (EPI == NMG_EPILOGUE_ADD) {
-                const _Float16 *rp = R + (int64_t)row * ldr + tok;
-                if (rvec && tok + 3 < N) {
-                    rr = *reinterpret_cast<const h4 *>(rp);
-                } else {
+            for (int i = 0; i < 4; ++i) {
+                const int row = r0 + 4 * q + i;
+                if (row >= M) continue;
 #pragma unroll
-                    for (int p = 0; p < 4; ++p)
-                        if (tok + p < N) rr[p] = rp[p];
+                for (int p = 0; p < TPL; ++p) {
+                    const int tok = t0 + 64 * p + lane;
+                    if (tok >= N) continue;
+                    const _Float16 h = (_Float16)acc[q][p][i];  // nearest even, as nmg_spmm stores it
+                    _Float16 out = h;
+                    if constexpr (E == NMG_EPILOGUE_GELU) {
+                        const uint16_t b = __builtin_bit_cast(uint16_t, h);
+                        const uint16_t *tab = reinterpret_cast<const uint16_t *>((b & 0x8000u) ? xs1 : xs0);
+                        out = __builtin_bit_cast(_Float16, tab[b & 0x7fffu]);
+                    } else if constexpr (E == NMG_EPILOGUE_ADD) {
+                        out = (_Float16)((float)h + (float)R[(int64_t)row * ldr + tok]);
+                    }
+                    __builtin_nontemporal_store(out, Y + (int64_t)row * ldy + tok);
                 }
             }
-            if (yvec && tok + 3 < N) {
-                const h4 v = {finish(acc[q][0][i], rr[0]), finish(acc[q][1][i], rr[1]),
-                              finish(acc[q][2][i], rr[2]), finish(acc[q][3][i], rr[3])};
-                __builtin_nontemporal_store(v, reinterpret_cast<h4 *>(y));
-                continue;
-            }
-#pragma unroll
-            for (int p = 0; p < 4; ++p)
-                if (tok + p < N) __builtin_nontemporal_store(finish(acc[q][p][i], rr[p]), y + p);
-        }
+    };
+    if (epi == NMG_EPILOGUE_GELU) store_all(std::integral_constant<int, NMG_EPILOGUE_GELU>{});
+    else if (epi == NMG_EPILOGUE_ADD) store_all(std::integral_constant<int, NMG_EPILOGUE_ADD>{});
+    else store_all(std::integral_constant<int, NMG_EPILOGUE_NONE>{});
 }
 
-// Largest window of 32, 16, 8 or 4 k-slots that n divides and whose chunks fit
-// the staging buffer; 0 if none.
-int half_window(const nmg_layout *L) {
-    for (int ksw = 32; ksw >= 4; ksw /= 2)
-        if (ksw % L->n == 0 && (ksw / L->n) * L->m <= kHalfWindowRows) return ksw;
+// Largest window of 4 .. 32 k-slots (64 with one token per lane: one A
+// register covers 64) that n divides and whose chunks fit the staging buffer;
+// 0 if none.
+int half_window(const nmg_layout *L, int tpl) {
+    for (int ksw = tpl == 1 ? 64 : 32; ksw >= 4; ksw /= 2)
+        if (ksw % L->n == 0 && (ksw / L->n) * L->m <= half_window_rows(tpl)) return ksw;
     return 0;
 }
 
-template <int U, int KSW, int EPI>
+// Tokens per lane: 4 (256-token tiles, fewer LDS reads per matrix instruction)
+// when the layer gives every SIMD two such waves; else 1 (64-token tiles: the
+// same waves then cover 4x the rows, so each staged X row feeds 4x the work)
+int half_tpl(const nmg_layout *L, int64_t N) {
+    const int64_t waves4 = (int64_t)((L->M + kHalfRowsWave - 1) / kHalfRowsWave) * ((N + 255) / 256);
+    return waves4 >= 8 * (int64_t)device_cus() && half_window(L, 4) ? 4 : 1;
+}
+
+template <int U, int KSW, int TPL>
 nmg_status launch_half(const SpmmArgs &a) {
     const nmg_layout *L = a.L;
-    const void *kern = reinterpret_cast<const void *>(&k_spmm_mfma_h<U, KSW, EPI>);
+    const void *kern = reinterpret_cast<const void *>(&k_spmm_mfma_h<U, KSW, TPL>);
     // waves per workgroup: the count whose tiles fill whole rounds of the GPU best
     const int cus = device_cus();
-    const int tok_tiles = (a.N + kHalfTokens - 1) / kHalfTokens;
+    const int tok_tiles = (a.N + 64 * TPL - 1) / (64 * TPL);
     int best_w = 4;
     double best_eff = -1.0;
     for (int w = 4; w <= kHalfMaxWaves; ++w) {
@@ -284,34 +298,32 @@ nmg_status launch_half(const SpmmArgs &a) {
     const int tiles = row_tiles * tok_tiles;
     const int64_t ldv = (int64_t)L->C * L->n;
     const bool avec = aligned(a.values, 8) && ldv % 4 == 0;
-    const bool yvec = aligned(a.Y, 8) && a.ldy % 4 == 0;
-    const bool rvec = a.R && aligned(a.R, 8) && a.ldr % 4 == 0;
     int log2n = 0;
     while ((1 << log2n) < L->n) ++log2n;
-    hipLaunchKernelGGL((k_spmm_mfma_h<U, KSW, EPI>), dim3(tiles), dim3(64 * best_w), 0, a.stream,
+    hipLaunchKernelGGL((k_spmm_mfma_h<U, KSW, TPL>), dim3(tiles), dim3(64 * best_w), 0, a.stream,
                        (const _Float16 *)a.values, a.indices, (const _Float16 *)a.X, a.ldx,
                        (_Float16 *)a.Y, a.ldy, (const _Float16 *)a.R, a.ldr, L->M, L->K, a.N,
-                       log2n, L->m, L->g, L->C, row_tiles, tiles, avec, yvec, rvec);
+                       log2n, L->m, L->g, L->C, row_tiles, tiles, (int)a.epi, avec);
     return launched();
-}
-
-template <int U, int KSW>
-nmg_status launch_half_e(const SpmmArgs &a) {
-    switch (a.epi) {
-        case NMG_EPILOGUE_NONE: return launch_half<U, KSW, NMG_EPILOGUE_NONE>(a);
-        case NMG_EPILOGUE_GELU: return launch_half<U, KSW, NMG_EPILOGUE_GELU>(a);
-        case NMG_EPILOGUE_ADD: return launch_half<U, KSW, NMG_EPILOGUE_ADD>(a);
-        default: return NMG_ERR_PARAM;
-    }
 }
 
 template <int U>
 nmg_status launch_half_u(const SpmmArgs &a) {
-    switch (half_window(a.L)) {
-        case 32: return launch_half_e<U, 32>(a);
-        case 16: return launch_half_e<U, 16>(a);
-        case 8: return launch_half_e<U, 8>(a);
-        case 4: return launch_half_e<U, 4>(a);
+    if (half_tpl(a.L, a.N) == 4) {
+        switch (half_window(a.L, 4)) {
+            case 32: return launch_half<U, 32, 4>(a);
+            case 16: return launch_half<U, 16, 4>(a);
+            case 8: return launch_half<U, 8, 4>(a);
+            case 4: return launch_half<U, 4, 4>(a);
+            default: return NMG_ERR_UNSUPPORTED;
+        }
+    }
+    switch (half_window(a.L, 1)) {
+        case 64: return launch_half<U, 64, 1>(a);
+        case 32: return launch_half<U, 32, 1>(a);
+        case 16: return launch_half<U, 16, 1>(a);
+        case 8: return launch_half<U, 8, 1>(a);
+        case 4: return launch_half<U, 4, 1>(a);
         default: return NMG_ERR_UNSUPPORTED;
     }
 }
@@ -326,7 +338,7 @@ nmg_status launch_half_u(const SpmmArgs &a) {
 bool nmg_internal::spmm_half_supported(const nmg_layout *L, const void *X, int64_t ldx, int64_t N) {
     const int64_t ldv = (int64_t)L->C * L->n;
     return L->dtype == NMG_F16 && mfma_unit(L) != 0 && (L->n & (L->n - 1)) == 0 &&
-           half_window(L) != 0 && (X == nullptr || aligned(X, 16)) && ldx % 8 == 0 && N % 8 == 0 &&
+           half_window(L, 1) != 0 && (X == nullptr || aligned(X, 16)) && ldx % 8 == 0 && N % 8 == 0 &&
            (int64_t)L->M * ldv < ((int64_t)1 << 31) && (int64_t)L->K * ldx < ((int64_t)1 << 31);
 }
 
