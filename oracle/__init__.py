@@ -16,6 +16,7 @@ reduce to library routines, or hand-worked examples.
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 import subprocess
 
@@ -69,12 +70,17 @@ def _load():
     lib.oracle_compress.argtypes = [i32, i64, i64, i32, i32, i32, vp, i64, vp, vp]
     lib.oracle_densify.argtypes = [i32, i64, i64, i32, i32, i32, vp, vp, vp, i64, vp]
     lib.oracle_repack.argtypes = [i32, i64, i64, i32, i32, i32, vp, i64, vp, vp]
+    lib.oracle_p_patterns.argtypes = [i32, i32, vp]
+    lib.oracle_p_compress.argtypes = [i32, i64, i64, i32, i32, i32, vp, i64, vp, vp]
+    lib.oracle_p_densify.argtypes = [i32, i64, i64, i32, i32, i32, vp, vp, vp, i64, vp]
+    lib.oracle_p_spmm.argtypes = [i32, i64, i64, i32, i32, i32, vp, vp, vp, i64, i64, vp, vp]
     lib.oracle_spmm.argtypes = [i32, i64, i64, i32, i32, i32, vp, vp, vp, i64, i64,
                                 vp, vp, i32]
     lib.oracle_spmm_points.argtypes = [i32, i64, i64, i32, i32, i32, vp, vp, vp, i64,
                                        i64, i64, vp, vp, vp, vp]
     for f in (lib.oracle_compress, lib.oracle_densify, lib.oracle_repack, lib.oracle_spmm,
-              lib.oracle_spmm_points):
+              lib.oracle_spmm_points, lib.oracle_p_patterns, lib.oracle_p_compress,
+              lib.oracle_p_densify, lib.oracle_p_spmm):
         f.restype = i32
     lib.oracle_half_to_float.argtypes = [ctypes.c_uint16]
     lib.oracle_half_to_float.restype = ctypes.c_float
@@ -259,3 +265,62 @@ def linear_stack_layer(x: np.ndarray, packed: dict, n: int, m: int, g: int):
     h = add_f16(x, lin("ao", vpart))
     u = gelu_f16(lin("up", h))
     return add_f16(h, lin("down", u))
+
+
+# ------------------------------------------------ the paper's chunked layout
+
+def p_patterns(m: int, n: int) -> np.ndarray:
+    """The C(m, n) patterns in revolving-door order (P x n offsets)."""
+    P = math.comb(m, n)
+    out = np.zeros((max(P, 1), n), dtype=np.uint8)
+    st = _load().oracle_p_patterns(m, n, _ptr(out))
+    if st:
+        raise OracleError(st, "p_patterns")
+    return out
+
+
+def p_compress(W: np.ndarray, n: int, m: int, g: int):
+    """Section 5.2 CPU converter into the chunked layout: (values, index).
+
+    values: M x (K/m * n), rows of each chunk in pattern order; index: M x (K/m)
+    uint8, the chunk row of the block at each position."""
+    W = np.ascontiguousarray(W)
+    dt = _dtype_code(W)
+    M, K = W.shape
+    B = K // m if m else 0
+    values = np.empty((M, B * n), dtype=W.dtype)
+    index = np.empty((M, B), dtype=np.uint8)
+    st = _load().oracle_p_compress(dt, M, K, n, m, g, _ptr(W), K, _ptr(values), _ptr(index))
+    if st:
+        raise OracleError(st, "p_compress")
+    return values, index
+
+
+def p_densify(values: np.ndarray, index: np.ndarray, K: int, n: int, m: int, g: int):
+    values = np.ascontiguousarray(values)
+    index = np.ascontiguousarray(index, dtype=np.uint8)
+    dt = _dtype_code(values)
+    M = values.shape[0]
+    out = np.empty((M, K), dtype=values.dtype)
+    mask = np.empty((M, K), dtype=np.uint8)
+    st = _load().oracle_p_densify(dt, M, K, n, m, g, _ptr(values), _ptr(index), _ptr(out), K,
+                                  _ptr(mask))
+    if st:
+        raise OracleError(st, "p_densify")
+    return out, mask.astype(bool)
+
+
+def p_spmm(values, index, X, K: int, n: int, m: int, g: int):
+    """Y = W_s X (binary64) for the chunked layout, and B = |W_s| |X|."""
+    values = np.ascontiguousarray(values)
+    index = np.ascontiguousarray(index, dtype=np.uint8)
+    X = np.ascontiguousarray(X)
+    dt = _dtype_code(values)
+    M, N = values.shape[0], X.shape[1]
+    Y = np.empty((M, N), dtype=np.float64)
+    Bnd = np.empty((M, N), dtype=np.float64)
+    st = _load().oracle_p_spmm(dt, M, K, n, m, g, _ptr(values), _ptr(index), _ptr(X), N, N,
+                               _ptr(Y), _ptr(Bnd))
+    if st:
+        raise OracleError(st, "p_spmm")
+    return Y, Bnd

@@ -398,3 +398,263 @@ void oracle_add_f16(const uint16_t *a, const uint16_t *b, uint16_t *out,
         out[i] = oracle_double_to_half((double)oracle_half_to_float(a[i]) +
                                        (double)oracle_half_to_float(b[i]));
 }
+
+/* ============================================ the paper's chunked layout */
+
+/* Section 5 of the paper, read literally ("Reading P"): besides repeating a
+ * pattern over a group, groups are combined into chunks that hold every one
+ * of the P = C(m, n) patterns in a fixed order, and the blocks of a chunk may
+ * be reordered, with an index recording each block's original place.
+ *   block    : m consecutive weights of one row along K; row r has K/m blocks
+ *              (K % m == 0 is required);
+ *   chunk    : the S = P*g blocks of S consecutive rows in one block column
+ *              (M % S == 0 and S <= 256 are required);
+ *   pattern  : an n-subset of the m offsets; the P patterns are listed in
+ *              revolving-door order, so adjacent patterns differ in one
+ *              position (Section 5.1: one register changes between groups);
+ *   group    : the g blocks of a chunk that use one pattern -- every pattern
+ *              is used by exactly g blocks of every chunk.
+ * Storage, with B = K/m block columns and the rows of a chunk in pattern
+ * order (positions j = 0 .. S-1, pattern j / g, rows of a group ascending):
+ *   values[c*S + j][b*n + s] = W[c*S + index[c*S + j][b]][b*m + pattern_{j/g}[s]]
+ *   index[c*S + j][b]        = the chunk row whose block sits at position j.
+ * Converter (Section 5.2, the CPU algorithm): every (row, pattern) pair of a
+ * chunk gets the magnitude its pattern keeps, summed in binary32 over the
+ * pattern's offsets in ascending order; the pairs are taken from the largest
+ * magnitude down (a NaN sum above every number; equal sums: lower pattern,
+ * then lower row, first), and a pair is used when its row has no pattern yet
+ * and its pattern has fewer than g rows. */
+
+static int64_t binom(int m, int n)
+{
+    int64_t v = 1;
+    for (int i = 1; i <= n; ++i) {
+        v = v * (m - n + i) / i;
+        if (v > 4096)
+            return 4097; /* more than any admissible layout */
+    }
+    return v;
+}
+
+/* Writes the revolving-door list of the n-subsets of {0 .. m-1} (each
+ * ascending) from `out`, returns the count:
+ *   list(m, n) = list(m-1, n), then list(m-1, n-1) reversed, each with m-1 added;
+ *   list(m, 0) = { {} };  list(m, m) = { {0 .. m-1} }. */
+static int64_t revolving_door(int m, int n, uint8_t *out)
+{
+    if (n == 0)
+        return 1;
+    if (n == m) {
+        for (int i = 0; i < n; ++i)
+            out[i] = (uint8_t)i;
+        return 1;
+    }
+    int64_t a = revolving_door(m - 1, n, out);
+    uint8_t *tail = out + a * n;
+    int64_t b = revolving_door(m - 1, n - 1, tail);
+    /* reverse the second list in place (patterns of n-1 offsets) and append m-1 */
+    uint8_t *tmp = (uint8_t *)malloc((size_t)(b * (n - 1) + 1));
+    memcpy(tmp, tail, (size_t)(b * (n - 1)));
+    for (int64_t i = 0; i < b; ++i) {
+        const uint8_t *src = tmp + (b - 1 - i) * (n - 1);
+        for (int s = 0; s < n - 1; ++s)
+            tail[i * n + s] = src[s];
+        tail[i * n + n - 1] = (uint8_t)(m - 1);
+    }
+    free(tmp);
+    return a + b;
+}
+
+int oracle_p_patterns(int m, int n, uint8_t *out)
+{
+    if (n < 1 || m < n || m > 255 || binom(m, n) > 256)
+        return ORC_EPARAM;
+    revolving_door(m, n, out);
+    return ORC_OK;
+}
+
+static int check_p_layout(int dtype, int64_t M, int64_t K, int n, int m, int g,
+                          int64_t *P, int64_t *S)
+{
+    if (dtype != ORC_F32 && dtype != ORC_F16)
+        return ORC_EPARAM;
+    if (M < 1 || K < 1 || n < 1 || m < n || m > 255 || g < 1)
+        return ORC_EPARAM;
+    *P = binom(m, n);
+    if (*P > 256)
+        return ORC_EPARAM;
+    *S = *P * g;
+    if (*S > 256 || K % m != 0 || M % *S != 0)
+        return ORC_ESHAPE;
+    return ORC_OK;
+}
+
+/* every chunk's index column is a permutation of 0 .. S-1 */
+static int check_p_index(int64_t M, int64_t B, int64_t S, const uint8_t *index)
+{
+    for (int64_t c = 0; c < M / S; ++c)
+        for (int64_t b = 0; b < B; ++b) {
+            uint8_t seen[256] = {0};
+            for (int64_t j = 0; j < S; ++j) {
+                int r = index[(c * S + j) * B + b];
+                if (r >= S || seen[r])
+                    return ORC_EINDEX;
+                seen[r] = 1;
+            }
+        }
+    return ORC_OK;
+}
+
+struct p_pair {
+    float score;
+    int p, r;
+};
+
+static int p_pair_order(const void *x, const void *y)
+{
+    const struct p_pair *a = (const struct p_pair *)x, *b = (const struct p_pair *)y;
+    if (score_above(a->score, b->score))
+        return -1;
+    if (score_above(b->score, a->score))
+        return 1;
+    if (a->p != b->p)
+        return a->p < b->p ? -1 : 1;
+    return a->r < b->r ? -1 : (a->r > b->r);
+}
+
+int oracle_p_compress(int dtype, int64_t M, int64_t K, int n, int m, int g,
+                      const void *W, int64_t ldw, void *values, uint8_t *index)
+{
+    int64_t P, S;
+    int st = check_p_layout(dtype, M, K, n, m, g, &P, &S);
+    if (st != ORC_OK)
+        return st;
+    if (ldw < K)
+        return ORC_EPARAM;
+    int64_t B = K / m, ldv = B * n;
+    uint8_t pat[256 * 255];
+    revolving_door(m, n, pat);
+    struct p_pair *pairs = (struct p_pair *)malloc(sizeof(struct p_pair) * (size_t)(S * P));
+    for (int64_t c = 0; c < M / S; ++c)
+        for (int64_t b = 0; b < B; ++b) {
+            /* the magnitude each pattern keeps for each row of the chunk */
+            for (int64_t r = 0; r < S; ++r)
+                for (int64_t p = 0; p < P; ++p) {
+                    float s = 0.0f;
+                    for (int i = 0; i < n; ++i)
+                        s = s + abs_elem32(dtype, W, ldw, c * S + r, b * m + pat[p * n + i]);
+                    pairs[r * P + p] = (struct p_pair){s, (int)p, (int)r};
+                }
+            qsort(pairs, (size_t)(S * P), sizeof(struct p_pair), p_pair_order);
+            int assigned[256], count[256];
+            for (int i = 0; i < 256; ++i) {
+                assigned[i] = -1;
+                count[i] = 0;
+            }
+            for (int64_t i = 0; i < S * P; ++i) {
+                const struct p_pair *q = &pairs[i];
+                if (assigned[q->r] < 0 && count[q->p] < g) {
+                    assigned[q->r] = q->p;
+                    ++count[q->p];
+                }
+            }
+            /* positions: patterns in order, rows of a group ascending */
+            int64_t j = 0;
+            for (int64_t p = 0; p < P; ++p)
+                for (int64_t r = 0; r < S; ++r)
+                    if (assigned[r] == p) {
+                        index[(c * S + j) * B + b] = (uint8_t)r;
+                        for (int i = 0; i < n; ++i)
+                            copy_elem(dtype, values, ldv, c * S + j, b * n + i, W, ldw, c * S + r,
+                                      b * m + pat[p * n + i]);
+                        ++j;
+                    }
+        }
+    free(pairs);
+    return ORC_OK;
+}
+
+int oracle_p_densify(int dtype, int64_t M, int64_t K, int n, int m, int g,
+                     const void *values, const uint8_t *index, void *W_out, int64_t ldw,
+                     uint8_t *mask)
+{
+    int64_t P, S;
+    int st = check_p_layout(dtype, M, K, n, m, g, &P, &S);
+    if (st != ORC_OK)
+        return st;
+    if (ldw < K)
+        return ORC_EPARAM;
+    int64_t B = K / m, ldv = B * n;
+    st = check_p_index(M, B, S, index);
+    if (st != ORC_OK)
+        return st;
+    uint8_t pat[256 * 255];
+    revolving_door(m, n, pat);
+    size_t sz = dtype == ORC_F32 ? 4 : 2;
+    for (int64_t r = 0; r < M; ++r) {
+        memset((char *)W_out + (size_t)(r * ldw) * sz, 0, (size_t)K * sz);
+        if (mask)
+            memset(mask + r * K, 0, (size_t)K);
+    }
+    for (int64_t c = 0; c < M / S; ++c)
+        for (int64_t b = 0; b < B; ++b)
+            for (int64_t j = 0; j < S; ++j) {
+                int64_t r = c * S + index[(c * S + j) * B + b], p = j / g;
+                for (int i = 0; i < n; ++i) {
+                    int64_t k = b * m + pat[p * n + i];
+                    copy_elem(dtype, W_out, ldw, r, k, values, ldv, c * S + j, b * n + i);
+                    if (mask)
+                        mask[r * K + k] = 1;
+                }
+            }
+    return ORC_OK;
+}
+
+/* Y = W_s X in binary64 for the chunked layout (the dense product with its
+ * zero terms left out, ascending column order per output row) and
+ * B = |W_s| |X|. */
+int oracle_p_spmm(int dtype, int64_t M, int64_t K, int n, int m, int g,
+                  const void *values, const uint8_t *index, const void *X, int64_t ldx,
+                  int64_t N, double *Y, double *Bnd)
+{
+    int64_t P, S;
+    int st = check_p_layout(dtype, M, K, n, m, g, &P, &S);
+    if (st != ORC_OK)
+        return st;
+    if (N < 1 || ldx < N)
+        return ORC_EPARAM;
+    int64_t B = K / m, ldv = B * n;
+    st = check_p_index(M, B, S, index);
+    if (st != ORC_OK)
+        return st;
+    uint8_t pat[256 * 255];
+    revolving_door(m, n, pat);
+    /* the position of every (row, block column) */
+    int64_t *pos = (int64_t *)malloc(sizeof(int64_t) * (size_t)(M * B));
+    for (int64_t c = 0; c < M / S; ++c)
+        for (int64_t b = 0; b < B; ++b)
+            for (int64_t j = 0; j < S; ++j)
+                pos[(c * S + index[(c * S + j) * B + b]) * B + b] = j;
+    for (int64_t r = 0; r < M; ++r) {
+        double *yr = Y + r * N, *br = Bnd + r * N;
+        for (int64_t t = 0; t < N; ++t) {
+            yr[t] = 0.0;
+            br[t] = 0.0;
+        }
+        int64_t c = r / S;
+        for (int64_t b = 0; b < B; ++b) {
+            int64_t j = pos[r * B + b], p = j / g;
+            for (int i = 0; i < n; ++i) {
+                int64_t k = b * m + pat[p * n + i];
+                double v = elem(dtype, values, ldv, c * S + j, b * n + i);
+                for (int64_t t = 0; t < N; ++t) {
+                    double x = elem(dtype, X, ldx, k, t);
+                    yr[t] += v * x;
+                    br[t] += fabs(v) * fabs(x);
+                }
+            }
+        }
+    }
+    free(pos);
+    return ORC_OK;
+}
