@@ -196,6 +196,59 @@ nmg_status nmg_gelu(nmg_dtype dtype, const void *in, void *out, int64_t count,
 nmg_status nmg_add(nmg_dtype dtype, const void *a, const void *b, void *out,
                    int64_t count, hipStream_t stream);
 
+/* ------------------------------------------------------------------------
+ * THE PAPER'S CHUNKED LAYOUT (Section 5, read literally).  Besides sharing a
+ * pattern over a group, blocks are combined into chunks that use every one of
+ * the P = C(m, n) patterns exactly g times, in revolving-door order (adjacent
+ * patterns differ in one position), and the blocks of a chunk are reordered
+ * by pattern with an index recording each block's row.
+ *   block   : m consecutive weights of a row along K (K % m == 0 required);
+ *   chunk   : the S = P * g blocks of S consecutive rows in one block column
+ *             (M % S == 0, S <= 256, P <= 256 required);
+ *   values  : M x (B * n), B = K / m; row c*S + j of chunk row-set c holds, in
+ *             block column b, the kept weights of the block at position j,
+ *             which uses pattern j / g (positions in pattern order, the rows of
+ *             a group ascending);
+ *   index   : M x B bytes; index[c*S + j][b] is the chunk row (0 .. S-1) of
+ *             the block at position j of block column b.
+ * nmg_p_compress follows the paper's CPU converter (Section 5.2): every
+ * (row, pattern) pair of a chunk is scored by the magnitude the pattern keeps
+ * (binary32, the pattern's offsets ascending, binary16 widened exactly), and
+ * pairs are taken from the largest down -- NaN above every number, equal
+ * scores to the lower pattern, then the lower row -- when the row has no
+ * pattern yet and the pattern has fewer than g rows.  A heuristic: it need not
+ * reach the largest kept magnitude.  The product and the conversion back follow
+ * the layout.  NMG_ERR_UNSUPPORTED when a chunk does not fit the kernels'
+ * LDS: S * P <= 8192, S * m <= 8192, P * n <= 4096. */
+typedef struct nmg_p_layout {
+    int32_t M, K;            /* dense weight is M x K                      */
+    int32_t n, m, g;
+    int32_t P, S, B;         /* patterns, rows per chunk, block columns    */
+    nmg_dtype dtype;
+} nmg_p_layout;
+
+/* Checks the parameters (NMG_ERR_PARAM), the shape rules above
+ * (NMG_ERR_SHAPE) and the dtype, and fills *layout.  Pure host code. */
+nmg_status nmg_p_layout_init(nmg_p_layout *layout, int32_t M, int32_t K, int32_t n,
+                             int32_t m, int32_t g, nmg_dtype dtype);
+
+/* Dense W (M x K, leading dimension ldw >= K, element-aligned) -> values and
+ * index; writes every entry of both. */
+nmg_status nmg_p_compress(const nmg_p_layout *layout, const void *W, int64_t ldw, void *values,
+                          uint8_t *index, hipStream_t stream);
+
+/* Y = W_s * X for the chunked layout: X K x N (ldx >= N), Y M x N (ldy >= N),
+ * element-aligned; binary32 accumulation in ascending column order of each
+ * row.  An index that is not a permutation in every chunk column gives
+ * unspecified Y, but no read leaves the buffers. */
+nmg_status nmg_p_spmm(const nmg_p_layout *layout, const void *values, const uint8_t *index,
+                      const void *X, int64_t ldx, int64_t N, void *Y, int64_t ldy,
+                      hipStream_t stream);
+
+/* Chunked layout -> dense W_out (M x K, leading dimension ldw >= K). */
+nmg_status nmg_p_densify(const nmg_p_layout *layout, const void *values, const uint8_t *index,
+                         void *W_out, int64_t ldw, hipStream_t stream);
+
 /* Static description of a status code; never NULL. */
 const char *nmg_status_str(nmg_status status);
 

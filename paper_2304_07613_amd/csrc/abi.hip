@@ -197,6 +197,62 @@ nmg_status nmg_spmm_epilogue(const nmg_layout *L, nmg_kernel kernel, nmg_epilogu
     return NMG_OK;
 }
 
+nmg_status nmg_p_layout_init(nmg_p_layout *layout, int32_t M, int32_t K, int32_t n, int32_t m,
+                             int32_t g, nmg_dtype dtype) {
+    if (!layout) return NMG_ERR_NULL;
+    if (dtype != NMG_F32 && dtype != NMG_F16) return NMG_ERR_DTYPE;
+    if (M < 1 || K < 1 || n < 1 || m < n || m > 255 || g < 1) return NMG_ERR_PARAM;
+    nmg_p_layout L;
+    L.M = M;
+    L.K = K;
+    L.n = n;
+    L.m = m;
+    L.g = g;
+    L.P = p_pattern_count(m, n);
+    if (L.P > 256) return NMG_ERR_PARAM;
+    L.S = L.P * g;
+    L.B = K / m;
+    L.dtype = dtype;
+    const nmg_status st = check_p_layout(&L);
+    if (st != NMG_OK) return st;
+    *layout = L;
+    return NMG_OK;
+}
+
+nmg_status nmg_p_compress(const nmg_p_layout *L, const void *W, int64_t ldw, void *values,
+                          uint8_t *index, hipStream_t stream) {
+    nmg_status st = check_p_layout(L);
+    if (st != NMG_OK) return st;
+    if (!W || !values || !index) return NMG_ERR_NULL;
+    if (ldw < L->K) return NMG_ERR_PARAM;
+    const size_t es = elem_size(L->dtype);
+    if (!aligned(W, es) || !aligned(values, es)) return NMG_ERR_ALIGN;
+    return launch_p_compress(L, W, ldw, values, index, stream);
+}
+
+nmg_status nmg_p_spmm(const nmg_p_layout *L, const void *values, const uint8_t *index,
+                      const void *X, int64_t ldx, int64_t N, void *Y, int64_t ldy,
+                      hipStream_t stream) {
+    nmg_status st = check_p_layout(L);
+    if (st != NMG_OK) return st;
+    if (!values || !index || !X || !Y) return NMG_ERR_NULL;
+    if (N < 1 || N > INT32_MAX || ldx < N || ldy < N) return NMG_ERR_PARAM;
+    const size_t es = elem_size(L->dtype);
+    if (!aligned(X, es) || !aligned(values, es) || !aligned(Y, es)) return NMG_ERR_ALIGN;
+    return launch_p_spmm(L, values, index, X, ldx, (int)N, Y, ldy, stream);
+}
+
+nmg_status nmg_p_densify(const nmg_p_layout *L, const void *values, const uint8_t *index,
+                         void *W_out, int64_t ldw, hipStream_t stream) {
+    nmg_status st = check_p_layout(L);
+    if (st != NMG_OK) return st;
+    if (!values || !index || !W_out) return NMG_ERR_NULL;
+    if (ldw < L->K) return NMG_ERR_PARAM;
+    const size_t es = elem_size(L->dtype);
+    if (!aligned(values, es) || !aligned(W_out, es)) return NMG_ERR_ALIGN;
+    return launch_p_densify(L, values, index, W_out, ldw, stream);
+}
+
 nmg_status nmg_spmm(const nmg_layout *L, const void *values, const uint8_t *indices,
                     const void *X, int64_t ldx, int64_t N, void *Y, int64_t ldy,
                     hipStream_t stream) {

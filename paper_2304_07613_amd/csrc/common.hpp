@@ -97,6 +97,16 @@ nmg_status spmm_scalar_f32_u4(const SpmmArgs &a);
 nmg_status spmm_scalar_f16(const SpmmArgs &a);
 
 bool spmm_half_supported(const nmg_layout *L, const void *X, int64_t ldx, int64_t N);
+
+nmg_status check_p_layout(const nmg_p_layout *L);
+int p_pattern_count(int m, int n);
+nmg_status launch_p_compress(const nmg_p_layout *L, const void *W, int64_t ldw, void *values,
+                             uint8_t *index, hipStream_t stream);
+nmg_status launch_p_densify(const nmg_p_layout *L, const void *values, const uint8_t *index,
+                            void *W_out, int64_t ldw, hipStream_t stream);
+nmg_status launch_p_spmm(const nmg_p_layout *L, const void *values, const uint8_t *index,
+                         const void *X, int64_t ldx, int N, void *Y, int64_t ldy,
+                         hipStream_t stream);
 nmg_status spmm_half(const SpmmArgs &a);
 
 }  // namespace nmg_internal

@@ -1,0 +1,297 @@
+// k_chunked.hip -- the paper's own chunked n:m:g layout (Section 5): chunks
+// of S = C(m,n) * g blocks that use every pattern exactly g times, in
+// revolving-door order, with the blocks reordered by pattern and an index of
+// their rows; the CPU converter of Section 5.2; the product; the conversion
+// back to dense.
+//
+//   k_p_compress  one workgroup per chunk: the magnitude every pattern keeps
+//                 for every row (binary32, the pattern's offsets ascending) in
+//                 LDS, then the greedy: S times, the largest pair whose row is
+//                 free and whose pattern has room (a workgroup max-reduction
+//                 of 64-bit keys: magnitude bits, then lower pattern, then
+//                 lower row) -- the same pairs, in the same order, as scanning
+//                 the sorted list of all pairs, since a pair that is not
+//                 eligible never becomes eligible again.
+//   k_p_spmm      vector FMAs: the rows of a group are scattered over the
+//                 chunk, so rows share no operands; each wave owns 16 rows of
+//                 one chunk and 256 tokens, and finds each row's position in
+//                 every block column through an inverse table built in LDS.
+//   k_p_densify   one thread per stored block.
+#include "common.hpp"
+
+namespace {
+
+constexpr int kPMaxS = 256;        // rows per chunk
+constexpr int kPMaxPairs = 8192;   // S * P scores held in LDS by the converter
+constexpr int kPMaxWblk = 8192;    // S * m weights of a chunk held in LDS
+constexpr int kPMaxPat = 4096;     // P * n pattern offsets held in LDS
+constexpr int kPRowsWave = 16;
+constexpr int kPTokens = 256;      // 4 per lane
+constexpr int kPWin = 32;          // block columns per inverse table
+
+__host__ __device__ inline int p_binom(int m, int n) {
+    int64_t v = 1;
+    for (int i = 1; i <= n; ++i) {
+        v = v * (m - n + i) / i;
+        if (v > 4096) return 4097;
+    }
+    return (int)v;
+}
+
+// Offsets (ascending) of pattern `idx` of the revolving-door list of the
+// n-subsets of {0 .. m-1}: the list of (m, n) is the list of (m-1, n)
+// followed by the list of (m-1, n-1) reversed, each with m-1 added; (m, m)
+// holds the single full set.  Unranked from the top: every binomial on the way
+// is at most C(m, n).
+__device__ void p_unrank(int m, int n, int idx, uint8_t *out) {
+    while (n > 0) {
+        if (n == m) {
+            for (int i = 0; i < n; ++i) out[i] = (uint8_t)i;
+            return;
+        }
+        const int first = p_binom(m - 1, n);
+        if (idx >= first) {  // in the second half: m-1 is in the pattern
+            idx = p_binom(m - 1, n - 1) - 1 - (idx - first);
+            out[n - 1] = (uint8_t)(m - 1);
+            --n;
+        }
+        --m;
+    }
+}
+
+template <typename T>
+__device__ __forceinline__ float p_abs(const T *p) { return fabsf((float)*p); }
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_p_compress(const T *__restrict__ W, int64_t ldw,
+                                                       T *__restrict__ values,
+                                                       uint8_t *__restrict__ index, int n, int m,
+                                                       int g, int P, int S, int B) {
+    using Bt = typename Bits<T>::type;
+    __shared__ float wabs[kPMaxWblk];
+    __shared__ float score[kPMaxPairs];
+    __shared__ uint8_t pat[kPMaxPat];
+    __shared__ int assigned[kPMaxS];
+    __shared__ int count[kPMaxS];
+    __shared__ unsigned long long best[kBlock / 64];
+    const int c = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
+    const int64_t row0 = (int64_t)c * S, ldv = (int64_t)B * n;
+
+    for (int i = t; i < S * m; i += kBlock)
+        wabs[i] = p_abs(W + (row0 + i / m) * ldw + (int64_t)b * m + i % m);
+    for (int p = t; p < P; p += kBlock) p_unrank(m, n, p, pat + p * n);
+    for (int r = t; r < S; r += kBlock) assigned[r] = -1;
+    for (int p = t; p < P; p += kBlock) count[p] = 0;
+    __syncthreads();
+    for (int i = t; i < S * P; i += kBlock) {
+        const int r = i / P, p = i % P;
+        float s = 0.f;  // binary32, the pattern's offsets ascending, from +0
+        for (int k = 0; k < n; ++k) s = s + wabs[r * m + pat[p * n + k]];
+        score[i] = s;
+    }
+    __syncthreads();
+
+    // key of pair (r, p): larger magnitude (NaN above all), then lower p, then lower r
+    auto key = [&](int i) -> unsigned long long {
+        const int r = i / P, p = i % P;
+        const float s = score[i];
+        const uint32_t bits = isnan(s) ? 0x7fc00000u : __builtin_bit_cast(uint32_t, s);
+        return ((unsigned long long)bits << 17) | (1ull << 16) | ((uint64_t)(255 - p) << 8) |
+               (uint64_t)(255 - r);
+    };
+    for (int it = 0; it < S; ++it) {
+        unsigned long long k = 0;
+        for (int i = t; i < S * P; i += kBlock) {
+            const int r = i / P, p = i % P;
+            if (assigned[r] < 0 && count[p] < g) k = max(k, key(i));
+        }
+        for (int off = 32; off > 0; off >>= 1) k = max(k, (unsigned long long)__shfl_xor(k, off));
+        if ((t & 63) == 0) best[t >> 6] = k;
+        __syncthreads();
+        if (t == 0) {
+            unsigned long long w = best[0];
+            for (int i = 1; i < kBlock / 64; ++i) w = max(w, best[i]);
+            // every step has a pair: the free rows equal the free pattern places
+            const int r = 255 - (int)(w & 0xff), p = 255 - (int)((w >> 8) & 0xff);
+            assigned[r] = p;
+            ++count[p];
+        }
+        __syncthreads();
+    }
+
+    // positions: patterns in order, rows of a group ascending; bit copies of W
+    for (int r = t; r < S; r += kBlock) {
+        const int p = assigned[r];
+        int pos = p * g;
+        for (int q = 0; q < r; ++q) pos += assigned[q] == p;
+        index[(row0 + pos) * B + b] = (uint8_t)r;
+        for (int k = 0; k < n; ++k)
+            reinterpret_cast<Bt *>(values)[(row0 + pos) * ldv + (int64_t)b * n + k] =
+                reinterpret_cast<const Bt *>(W)[(row0 + r) * ldw + (int64_t)b * m + pat[p * n + k]];
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_p_densify(const T *__restrict__ values,
+                                                      const uint8_t *__restrict__ index,
+                                                      T *__restrict__ out, int64_t ldw, int M,
+                                                      int n, int m, int g, int P, int S, int B) {
+    using Bt = typename Bits<T>::type;
+    __shared__ uint8_t pat[kPMaxPat];
+    for (int p = threadIdx.x; p < P; p += kBlock) p_unrank(m, n, p, pat + p * n);
+    __syncthreads();
+    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;  // (stored row, block column)
+    if (i >= (int64_t)M * B) return;
+    const int64_t R = i / B;
+    const int b = (int)(i % B);
+    const int j = (int)(R % S);
+    const int64_t r = R - j + min((int)index[R * B + b], S - 1);  // chunk row, clamped
+    const uint8_t *off = pat + (j / g) * n;
+    Bt *o = reinterpret_cast<Bt *>(out) + r * ldw + (int64_t)b * m;
+    for (int k = 0; k < m; ++k) o[k] = 0;
+    const Bt *v = reinterpret_cast<const Bt *>(values) + R * ((int64_t)B * n) + (int64_t)b * n;
+    for (int k = 0; k < n; ++k) o[off[k]] = v[k];
+}
+
+constexpr int kPMaxWaves = kPMaxS / kPRowsWave;  // 16 waves cover the largest chunk
+
+template <typename T>
+__global__ __launch_bounds__(64 * kPMaxWaves) void k_p_spmm(const T *__restrict__ values,
+                                                   const uint8_t *__restrict__ index,
+                                                   const T *__restrict__ X, int64_t ldx,
+                                                   T *__restrict__ Y, int64_t ldy, int N, int n,
+                                                   int m, int g, int P, int S, int B, int tok_tiles,
+                                                   bool xvec) {
+    __shared__ uint8_t pat[kPMaxPat];
+    __shared__ uint8_t inv[kPWin * kPMaxS];  // position of chunk row rr in block column w
+    const int c = blockIdx.x / tok_tiles, tt = blockIdx.x % tok_tiles;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t row0 = (int64_t)c * S, ldv = (int64_t)B * n;
+    const int tok = tt * kPTokens + 4 * lane;
+    const int valid = N - tok;
+    const int rr0 = wave * kPRowsWave;  // this wave's first chunk row
+
+    for (int p = threadIdx.x; p < P; p += blockDim.x) p_unrank(m, n, p, pat + p * n);
+
+    float acc[kPRowsWave][4];
+#pragma unroll
+    for (int r = 0; r < kPRowsWave; ++r)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[r][j] = 0.f;
+
+    for (int b0 = 0; b0 < B; b0 += kPWin) {
+        const int nb = min(kPWin, B - b0);
+        __syncthreads();  // the previous window's table is no longer read
+        for (int i = threadIdx.x; i < nb * S; i += blockDim.x) {
+            const int w = i / S, jpos = i % S;
+            const int rr = min((int)index[(row0 + jpos) * B + b0 + w], S - 1);
+            inv[w * kPMaxS + rr] = (uint8_t)jpos;
+        }
+        __syncthreads();
+        for (int w = 0; w < nb; ++w) {
+            const int b = b0 + w;
+#pragma unroll
+            for (int r = 0; r < kPRowsWave; ++r) {
+                const int rr = rr0 + r;
+                if (rr >= S) continue;
+                const int jpos = min((int)inv[w * kPMaxS + rr], S - 1);  // clamped: malformed
+                                                                          // indices stay inside
+                const uint8_t *off = pat + (jpos / g) * n;
+                const T *v = values + (row0 + jpos) * ldv + (int64_t)b * n;
+                for (int k = 0; k < n; ++k) {
+                    const float wv = (float)v[k];
+                    const v4f x = load4<T>(X + ((int64_t)b * m + off[k]) * ldx + tok, valid, xvec);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[r][j] = fmaf(wv, x[j], acc[r][j]);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < kPRowsWave; ++r) {
+        const int rr = rr0 + r;
+        if (rr >= S) continue;
+        T *y = Y + (row0 + rr) * ldy + tok;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (j < valid) y[j] = (T)acc[r][j];
+    }
+}
+
+bool p_fits(const nmg_p_layout *L) {
+    return L->S * L->P <= kPMaxPairs && L->S * L->m <= kPMaxWblk && L->P * L->n <= kPMaxPat &&
+           L->S <= kPMaxS;
+}
+
+}  // namespace
+
+namespace nmg_internal {
+
+nmg_status check_p_layout(const nmg_p_layout *L) {
+    if (!L) return NMG_ERR_NULL;
+    if (L->dtype != NMG_F32 && L->dtype != NMG_F16) return NMG_ERR_DTYPE;
+    if (L->M < 1 || L->K < 1 || L->n < 1 || L->m < L->n || L->m > 255 || L->g < 1)
+        return NMG_ERR_PARAM;
+    const int P = p_binom(L->m, L->n);
+    if (P > 256 || L->P != P || L->S != P * L->g || L->B != L->K / L->m) return NMG_ERR_PARAM;
+    if (L->S > kPMaxS || L->K % L->m != 0 || L->M % L->S != 0) return NMG_ERR_SHAPE;
+    return NMG_OK;
+}
+
+int p_pattern_count(int m, int n) { return p_binom(m, n); }
+
+nmg_status launch_p_compress(const nmg_p_layout *L, const void *W, int64_t ldw, void *values,
+                             uint8_t *index, hipStream_t stream) {
+    if (!p_fits(L)) return NMG_ERR_UNSUPPORTED;
+    dim3 grid(L->M / L->S, L->B);
+    if (L->dtype == NMG_F32)
+        hipLaunchKernelGGL((k_p_compress<float>), grid, dim3(kBlock), 0, stream, (const float *)W,
+                           ldw, (float *)values, index, L->n, L->m, L->g, L->P, L->S, L->B);
+    else
+        hipLaunchKernelGGL((k_p_compress<_Float16>), grid, dim3(kBlock), 0, stream,
+                           (const _Float16 *)W, ldw, (_Float16 *)values, index, L->n, L->m, L->g,
+                           L->P, L->S, L->B);
+    return launched();
+}
+
+nmg_status launch_p_densify(const nmg_p_layout *L, const void *values, const uint8_t *index,
+                            void *W_out, int64_t ldw, hipStream_t stream) {
+    if (!p_fits(L)) return NMG_ERR_UNSUPPORTED;
+    const int64_t blocks = ((int64_t)L->M * L->B + kBlock - 1) / kBlock;
+    if (blocks > INT32_MAX) return NMG_ERR_PARAM;
+    if (L->dtype == NMG_F32)
+        hipLaunchKernelGGL((k_p_densify<float>), dim3((unsigned)blocks), dim3(kBlock), 0, stream,
+                           (const float *)values, index, (float *)W_out, ldw, L->M, L->n, L->m,
+                           L->g, L->P, L->S, L->B);
+    else
+        hipLaunchKernelGGL((k_p_densify<_Float16>), dim3((unsigned)blocks), dim3(kBlock), 0,
+                           stream, (const _Float16 *)values, index, (_Float16 *)W_out, ldw, L->M,
+                           L->n, L->m, L->g, L->P, L->S, L->B);
+    return launched();
+}
+
+nmg_status launch_p_spmm(const nmg_p_layout *L, const void *values, const uint8_t *index,
+                         const void *X, int64_t ldx, int N, void *Y, int64_t ldy,
+                         hipStream_t stream) {
+    if (!p_fits(L)) return NMG_ERR_UNSUPPORTED;
+    const int tok_tiles = (N + kPTokens - 1) / kPTokens;
+    const int64_t grid = (int64_t)(L->M / L->S) * tok_tiles;
+    if (grid > INT32_MAX) return NMG_ERR_PARAM;
+    const int waves = (L->S + kPRowsWave - 1) / kPRowsWave;
+    // binary32 X rows on 16-byte boundaries are read 4 tokens at a time
+    const size_t es = elem_size(L->dtype);
+    const bool xvec = aligned(X, 4 * es) && ldx % 4 == 0;
+    if (L->dtype == NMG_F32)
+        hipLaunchKernelGGL((k_p_spmm<float>), dim3((unsigned)grid), dim3(64 * waves), 0, stream,
+                           (const float *)values, index, (const float *)X, ldx, (float *)Y, ldy, N,
+                           L->n, L->m, L->g, L->P, L->S, L->B, tok_tiles, xvec);
+    else
+        hipLaunchKernelGGL((k_p_spmm<_Float16>), dim3((unsigned)grid), dim3(64 * waves), 0,
+                           stream, (const _Float16 *)values, index, (const _Float16 *)X, ldx,
+                           (_Float16 *)Y, ldy, N, L->n, L->m, L->g, L->P, L->S, L->B, tok_tiles,
+                           xvec);
+    return launched();
+}
+
+}  // namespace nmg_internal

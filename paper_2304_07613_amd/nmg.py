@@ -43,6 +43,12 @@ class _Layout(ctypes.Structure):
                 ("dtype", ctypes.c_int)]
 
 
+class _PLayout(ctypes.Structure):
+    _fields_ = [("M", ctypes.c_int32), ("K", ctypes.c_int32), ("n", ctypes.c_int32),
+                ("m", ctypes.c_int32), ("g", ctypes.c_int32), ("P", ctypes.c_int32),
+                ("S", ctypes.c_int32), ("B", ctypes.c_int32), ("dtype", ctypes.c_int)]
+
+
 _lib = None
 
 
@@ -62,6 +68,7 @@ def lib():
         raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
     L = ctypes.CDLL(LIB_PATH)
     vp, i64, i32, lp = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.POINTER(_Layout)
+    pp = ctypes.POINTER(_PLayout)
     sig = {
         "nmg_layout_init": ([lp, i32, i32, i32, i32, i32, ctypes.c_int], ctypes.c_int),
         "nmg_values_numel": ([lp], i64),
@@ -76,6 +83,10 @@ def lib():
         "nmg_densify": ([lp, vp, vp, vp, i64, vp], ctypes.c_int),
         "nmg_gelu": ([ctypes.c_int, vp, vp, i64, vp], ctypes.c_int),
         "nmg_add": ([ctypes.c_int, vp, vp, vp, i64, vp], ctypes.c_int),
+        "nmg_p_layout_init": ([pp, i32, i32, i32, i32, i32, ctypes.c_int], ctypes.c_int),
+        "nmg_p_compress": ([pp, vp, i64, vp, vp, vp], ctypes.c_int),
+        "nmg_p_spmm": ([pp, vp, vp, vp, i64, i64, vp, i64, vp], ctypes.c_int),
+        "nmg_p_densify": ([pp, vp, vp, vp, i64, vp], ctypes.c_int),
         "nmg_status_str": ([ctypes.c_int], ctypes.c_char_p),
         "nmg_version": ([], ctypes.c_char_p),
     }
@@ -278,4 +289,78 @@ def add(a: torch.Tensor, b: torch.Tensor, out: torch.Tensor | None = None):
     out = torch.empty_like(a) if out is None else out
     _check(lib().nmg_add(_DTYPE_CODE[a.dtype], _ptr(a), _ptr(b), _ptr(out), a.numel(),
                          _stream(a)), "nmg_add")
+    return out
+
+
+# ------------------------------------------------ the paper's chunked layout
+
+class PLayout:
+    """Shape of one weight in the paper's chunked layout (``nmg_p_layout``)."""
+
+    def __init__(self, M: int, K: int, n: int, m: int, g: int, dtype=torch.float32):
+        if dtype not in _DTYPE_CODE:
+            raise TypeError(f"unsupported dtype {dtype}")
+        self.c = _PLayout()
+        _check(lib().nmg_p_layout_init(ctypes.byref(self.c), M, K, n, m, g, _DTYPE_CODE[dtype]),
+               "nmg_p_layout_init")
+        self.dtype = dtype
+
+    M = property(lambda s: s.c.M)
+    K = property(lambda s: s.c.K)
+    n = property(lambda s: s.c.n)
+    m = property(lambda s: s.c.m)
+    g = property(lambda s: s.c.g)
+    P = property(lambda s: s.c.P)
+    S = property(lambda s: s.c.S)
+    B = property(lambda s: s.c.B)
+
+    @property
+    def values_shape(self):
+        return (self.M, self.B * self.n)
+
+    @property
+    def index_shape(self):
+        return (self.M, self.B)
+
+
+def p_compress(W: torch.Tensor, n: int, m: int, g: int):
+    """Dense W (M x K, GPU) -> (values, index, layout) in the chunked layout."""
+    _need_cuda(W)
+    layout = PLayout(W.shape[0], W.shape[1], n, m, g, W.dtype)
+    values = torch.empty(layout.values_shape, dtype=W.dtype, device=W.device)
+    index = torch.empty(layout.index_shape, dtype=torch.uint8, device=W.device)
+    _check(lib().nmg_p_compress(ctypes.byref(layout.c), _ptr(W), _rows(W, "W"), _ptr(values),
+                                _ptr(index), _stream(W)), "nmg_p_compress")
+    return values, index, layout
+
+
+def _p_check(layout: PLayout, values, index):
+    _need_cuda(values, index)
+    if values.dtype != layout.dtype or index.dtype != torch.uint8:
+        raise TypeError("dtype mismatch")
+    if tuple(values.shape) != layout.values_shape or not values.is_contiguous():
+        raise ValueError(f"values must be contiguous {layout.values_shape}")
+    if tuple(index.shape) != layout.index_shape or not index.is_contiguous():
+        raise ValueError(f"index must be contiguous {layout.index_shape}")
+
+
+def p_spmm(values, index, X, layout: PLayout):
+    """Y = W_s X for the chunked layout."""
+    _p_check(layout, values, index)
+    _need_cuda(X)
+    if X.dtype != layout.dtype or X.shape[0] != layout.K:
+        raise ValueError("X must be K x N of the layout's dtype")
+    Y = torch.empty((layout.M, X.shape[1]), dtype=X.dtype, device=X.device)
+    _check(lib().nmg_p_spmm(ctypes.byref(layout.c), _ptr(values), _ptr(index), _ptr(X),
+                            _rows(X, "X"), X.shape[1], _ptr(Y), _rows(Y, "Y"), _stream(X)),
+           "nmg_p_spmm")
+    return Y
+
+
+def p_densify(values, index, layout: PLayout):
+    """Chunked layout -> dense M x K weight."""
+    _p_check(layout, values, index)
+    out = torch.empty((layout.M, layout.K), dtype=layout.dtype, device=values.device)
+    _check(lib().nmg_p_densify(ctypes.byref(layout.c), _ptr(values), _ptr(index), _ptr(out),
+                               layout.K, _stream(values)), "nmg_p_densify")
     return out

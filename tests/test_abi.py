@@ -112,3 +112,25 @@ def test_binding_refuses_cpu_tensors(lib):
     W = torch.zeros(8, 8)
     with pytest.raises(ValueError):
         nmg.compress(W, 1, 4, 4)
+
+
+def test_chunked_layout_validation(lib):
+    import ctypes
+    L = nmg._PLayout()
+    assert lib.nmg_p_layout_init(ctypes.byref(L), 3072, 768, 1, 4, 8, nmg.F32) == nmg.OK
+    assert (L.P, L.S, L.B) == (4, 32, 192)
+    assert lib.nmg_p_layout_init(ctypes.byref(L), 3072, 768, 2, 8, 8, nmg.F32) == nmg.ERR_SHAPE  # 224 rows
+    assert lib.nmg_p_layout_init(ctypes.byref(L), 768, 770, 2, 4, 4, nmg.F32) == nmg.ERR_SHAPE   # K % m
+    assert lib.nmg_p_layout_init(ctypes.byref(L), 924, 12, 6, 12, 1, nmg.F32) == nmg.ERR_PARAM   # 924 patterns
+    assert lib.nmg_p_layout_init(ctypes.byref(L), 512, 8, 1, 4, 128, nmg.F32) == nmg.ERR_SHAPE  # S = 512
+    assert lib.nmg_p_layout_init(None, 8, 8, 1, 4, 2, nmg.F32) == nmg.ERR_NULL
+    assert lib.nmg_p_layout_init(ctypes.byref(L), 48, 16, 2, 4, 2, nmg.F16) == nmg.OK
+    p, s = ctypes.c_void_p(1 << 20), ctypes.c_void_p(0)
+    odd = ctypes.c_void_p((1 << 20) + 1)
+    assert lib.nmg_p_compress(ctypes.byref(L), p, 15, p, p, s) == nmg.ERR_PARAM     # ldw < K
+    assert lib.nmg_p_compress(ctypes.byref(L), None, 16, p, p, s) == nmg.ERR_NULL
+    assert lib.nmg_p_compress(ctypes.byref(L), odd, 16, p, p, s) == nmg.ERR_ALIGN
+    assert lib.nmg_p_spmm(ctypes.byref(L), p, p, p, 8, 16, p, 16, s) == nmg.ERR_PARAM  # ldx < N
+    assert lib.nmg_p_densify(ctypes.byref(L), p, None, p, 16, s) == nmg.ERR_NULL
+    bad = nmg._PLayout(48, 16, 2, 4, 2, 6, 10, 4, nmg.F16)   # S inconsistent with P * g
+    assert lib.nmg_p_compress(ctypes.byref(bad), p, 16, p, p, s) == nmg.ERR_PARAM

@@ -419,3 +419,78 @@ def test_elementwise_glue(nmg):
     from scipy.special import erf
     xd = np_of(x32).astype(np.float64)
     assert np.allclose(g32, 0.5 * xd * (1 + erf(xd / np.sqrt(2))), rtol=1e-6, atol=1e-7)
+
+
+# ------------------------------------------- the paper's chunked layout
+
+P_SHAPES = [
+    # M,    K,   N,    n, m, g,  dtype
+    (48, 16, 100, 2, 4, 2, torch.float32),
+    (96, 40, 256, 1, 4, 8, torch.float16),
+    (120, 60, 77, 3, 6, 1, torch.float32),      # ragged N
+    (192, 48, 64, 2, 4, 32, torch.float32),     # S = 192
+    (256, 32, 40, 1, 4, 64, torch.float16),     # S = 256, one chunk row-set
+    (224, 16, 33, 2, 8, 8, torch.float32),      # 28 patterns, S = 224
+    (768, 768, 128, 2, 4, 4, torch.float32),    # the single-layer shape
+]
+
+
+@pytest.mark.parametrize("M,K,N,n,m,g,dtype", P_SHAPES,
+                         ids=[f"{c[0]}x{c[1]}x{c[2]}-{c[3]}:{c[4]}:{c[5]}-{str(c[6])[6:]}"
+                              for c in P_SHAPES])
+def test_chunked_layout(nmg, M, K, N, n, m, g, dtype):
+    W = synth.normal((M, K), 81 + M, 0.02, dtype)
+    X = synth.normal((K, N), 82 + N, 1.0, dtype)
+    print(f"[chunked] {M}x{K}x{N} {n}:{m}:{g} {dtype}", flush=True)
+    v, idx, L = nmg.p_compress(W.to(DEV), n, m, g)
+    torch.cuda.synchronize()
+    rv, ridx = oracle.p_compress(np_of(W), n, m, g)
+    assert np.array_equal(np_of(idx), ridx), f"index differs at {np.argwhere(np_of(idx) != ridx)[:5]}"
+    assert np.array_equal(bits(np_of(v)), bits(rv))
+    dense = nmg.p_densify(v, idx, L)
+    rd, _ = oracle.p_densify(rv, ridx, K, n, m, g)
+    assert np.array_equal(bits(np_of(dense)), bits(rd))
+    Y = nmg.p_spmm(v, idx, X.to(DEV), L)
+    torch.cuda.synchronize()
+    Yref, B = oracle.p_spmm(rv, ridx, np_of(X), K, n, m, g)
+    check_product(Y, Yref, B, dtype, "chunked")
+
+
+def test_chunked_layout_ties_and_nan(nmg):
+    rng = np.random.default_rng(5)
+    W = (rng.integers(-3, 4, size=(96, 24)) / 2.0).astype(np.float32)   # many equal magnitudes
+    W[5, 3] = np.nan
+    W[40:50, 8:12] = -0.0
+    for n, m, g in [(2, 4, 4), (1, 4, 8), (1, 2, 6), (3, 6, 1)]:
+        if 96 % (math_comb(m, n) * g) or 24 % m:
+            continue
+        print(f"[chunked ties] {n}:{m}:{g}", flush=True)
+        v, idx, L = nmg.p_compress(torch.from_numpy(W).to(DEV), n, m, g)
+        torch.cuda.synchronize()
+        rv, ridx = oracle.p_compress(W, n, m, g)
+        assert np.array_equal(np_of(idx), ridx)
+        assert np.array_equal(bits(np_of(v)), bits(rv))
+
+
+def math_comb(m, n):
+    import math
+    return math.comb(m, n)
+
+
+def test_chunked_layout_ffn_shape(nmg):
+    """The FFN up-projection shape (3072 x 768, 1:4:8 -> chunks of 32 rows) with
+    4096 tokens: packing bit-exact, products checked on 192 whole rows."""
+    lin = synth.WORKLOADS[2].layers[0]
+    W, X = synth.layer_inputs(2, 0, lin)
+    v, idx, L = nmg.p_compress(W.to(DEV), 1, 4, 8)
+    torch.cuda.synchronize()
+    rv, ridx = oracle.p_compress(np_of(W), 1, 4, 8)
+    assert np.array_equal(np_of(idx), ridx) and np.array_equal(bits(np_of(v)), bits(rv))
+    Y = nmg.p_spmm(v, idx, X.to(DEV), L)
+    torch.cuda.synchronize()
+    rd, _ = oracle.p_densify(rv, ridx, lin.K, 1, 4, 8)
+    rows = np.random.default_rng(9).choice(lin.M, 192, replace=False)
+    Xd = np_of(X).astype(np.float64)
+    Yref = rd[rows].astype(np.float64) @ Xd
+    B = np.abs(rd[rows].astype(np.float64)) @ np.abs(Xd)
+    check_product(Y[torch.as_tensor(rows, device=Y.device)], Yref, B, torch.float32, "chunked ffn")
