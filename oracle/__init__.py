@@ -74,13 +74,14 @@ def _load():
     lib.oracle_p_compress.argtypes = [i32, i64, i64, i32, i32, i32, vp, i64, vp, vp]
     lib.oracle_p_densify.argtypes = [i32, i64, i64, i32, i32, i32, vp, vp, vp, i64, vp]
     lib.oracle_p_spmm.argtypes = [i32, i64, i64, i32, i32, i32, vp, vp, vp, i64, i64, vp, vp]
+    lib.oracle_p_refine.argtypes = [i32, i64, i64, i32, i32, i32, vp, i64, vp, vp, vp]
     lib.oracle_spmm.argtypes = [i32, i64, i64, i32, i32, i32, vp, vp, vp, i64, i64,
                                 vp, vp, i32]
     lib.oracle_spmm_points.argtypes = [i32, i64, i64, i32, i32, i32, vp, vp, vp, i64,
                                        i64, i64, vp, vp, vp, vp]
     for f in (lib.oracle_compress, lib.oracle_densify, lib.oracle_repack, lib.oracle_spmm,
               lib.oracle_spmm_points, lib.oracle_p_patterns, lib.oracle_p_compress,
-              lib.oracle_p_densify, lib.oracle_p_spmm):
+              lib.oracle_p_densify, lib.oracle_p_spmm, lib.oracle_p_refine):
         f.restype = i32
     lib.oracle_half_to_float.argtypes = [ctypes.c_uint16]
     lib.oracle_half_to_float.restype = ctypes.c_float
@@ -324,3 +325,19 @@ def p_spmm(values, index, X, K: int, n: int, m: int, g: int):
     if st:
         raise OracleError(st, "p_spmm")
     return Y, Bnd
+
+
+def p_refine(W: np.ndarray, index: np.ndarray, n: int, m: int, g: int):
+    """The swap search of Section 5.2 from the packing `index` (this module's
+    fixed-order reading): returns (values, index, rounds of the slowest chunk)."""
+    W = np.ascontiguousarray(W)
+    dt = _dtype_code(W)
+    M, K = W.shape
+    idx = np.array(index, dtype=np.uint8, copy=True, order="C")
+    values = np.empty((M, (K // m) * n), dtype=W.dtype)
+    rounds = ctypes.c_int(0)
+    st = _load().oracle_p_refine(dt, M, K, n, m, g, _ptr(W), K, _ptr(values), _ptr(idx),
+                                 ctypes.byref(rounds))
+    if st:
+        raise OracleError(st, "p_refine")
+    return values, idx, rounds.value

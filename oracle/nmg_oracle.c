@@ -658,3 +658,101 @@ int oracle_p_spmm(int dtype, int64_t M, int64_t K, int n, int m, int g,
     free(pos);
     return ORC_OK;
 }
+
+/* The paper's GPU converter (Section 5.2) as a refinement of a packing: the
+ * blocks of a chunk hold patterns; a swap of the patterns of two blocks with
+ * different patterns is made when it raises the magnitude the pair keeps,
+ * until no swap does.  The paper lets threads race for swaps; this reading
+ * fixes an order.  In every round each row finds its best partner -- the
+ * largest gain s(r,b) + s(r',a) - s(r,a) - s(r',b) > 0, sums in binary64 of
+ * the binary32 magnitudes, ties to the lower partner row; every pair of
+ * mutual best partners swaps.  (Gains are symmetric, so while any swap
+ * improves there is a mutual pair: the lowest row of a pair with the largest
+ * gain and its lowest such partner.)  Rounds end when no swap improves, or
+ * after 8 * S rounds.  The
+ * result is stored like nmg_p_compress's (patterns in order, rows of a group
+ * ascending), values copied from W. */
+static double p_gain(const float *sc, int64_t P, int r, int a, int q, int b)
+{
+    return ((double)sc[r * P + b] + (double)sc[q * P + a]) -
+           ((double)sc[r * P + a] + (double)sc[q * P + b]);
+}
+
+int oracle_p_refine(int dtype, int64_t M, int64_t K, int n, int m, int g, const void *W,
+                    int64_t ldw, void *values, uint8_t *index, int *rounds_out)
+{
+    int64_t P, S;
+    int st = check_p_layout(dtype, M, K, n, m, g, &P, &S);
+    if (st != ORC_OK)
+        return st;
+    if (ldw < K)
+        return ORC_EPARAM;
+    int64_t B = K / m, ldv = B * n;
+    st = check_p_index(M, B, S, index);
+    if (st != ORC_OK)
+        return st;
+    uint8_t pat[256 * 255];
+    revolving_door(m, n, pat);
+    float *sc = (float *)malloc(sizeof(float) * (size_t)(S * P));
+    int max_rounds = 0;
+    for (int64_t c = 0; c < M / S; ++c)
+        for (int64_t b = 0; b < B; ++b) {
+            for (int64_t r = 0; r < S; ++r)
+                for (int64_t p = 0; p < P; ++p) {
+                    float s = 0.0f;
+                    for (int i = 0; i < n; ++i)
+                        s = s + abs_elem32(dtype, W, ldw, c * S + r, b * m + pat[p * n + i]);
+                    sc[r * P + p] = s;
+                }
+            int pa[256], best[256];
+            double bg[256];
+            for (int64_t j = 0; j < S; ++j)
+                pa[index[(c * S + j) * B + b]] = (int)(j / g);
+            int round = 0;
+            for (; round < 8 * S; ++round) {
+                int any = 0;
+                for (int r = 0; r < S; ++r) {
+                    best[r] = -1;
+                    bg[r] = 0.0;
+                    for (int q = 0; q < S; ++q) {
+                        if (pa[q] == pa[r])
+                            continue;
+                        double gq = p_gain(sc, P, r, pa[r], q, pa[q]);
+                        if (gq > bg[r]) { /* strictly larger: ties keep the lower q */
+                            bg[r] = gq;
+                            best[r] = q;
+                        }
+                    }
+                    any |= best[r] >= 0;
+                }
+                if (!any)
+                    break;
+                int newpa[256];
+                memcpy(newpa, pa, sizeof(int) * (size_t)S);
+                for (int r = 0; r < S; ++r) {
+                    int q = best[r];
+                    if (q > r && best[q] == r) { /* mutual best partners: disjoint pairs */
+                        newpa[r] = pa[q];
+                        newpa[q] = pa[r];
+                    }
+                }
+                memcpy(pa, newpa, sizeof(int) * (size_t)S);
+            }
+            if (round > max_rounds)
+                max_rounds = round;
+            int64_t j = 0;
+            for (int64_t p = 0; p < P; ++p)
+                for (int64_t r = 0; r < S; ++r)
+                    if (pa[r] == p) {
+                        index[(c * S + j) * B + b] = (uint8_t)r;
+                        for (int i = 0; i < n; ++i)
+                            copy_elem(dtype, values, ldv, c * S + j, b * n + i, W, ldw, c * S + r,
+                                      b * m + pat[p * n + i]);
+                        ++j;
+                    }
+        }
+    free(sc);
+    if (rounds_out)
+        *rounds_out = max_rounds;
+    return ORC_OK;
+}

@@ -145,3 +145,63 @@ def test_rejections():
     with pytest.raises(oracle.OracleError) as e:
         oracle.p_densify(values, bad, 8, 2, 4, 4)
     assert e.value.status == 3
+
+
+# ------------------------------------------------------------ swap search
+
+def kept(values):
+    return float(np.abs(values.astype(np.float64)).sum())
+
+
+def test_refine_fixes_the_hand_example():
+    """Golden case 2: the greedy keeps 3 of the optimum 5; one swap (gain
+    2 + 3 - 3 - 0 = 2) reaches it."""
+    gold = json.load(open(os.path.join(GOLDEN, "chunked_greedy.json")))["cases"][1]
+    W = np.array(gold["W"], np.float32)
+    values, index = oracle.p_compress(W, 1, 2, 1)
+    rv, ridx, rounds = oracle.p_refine(W, index, 1, 2, 1)
+    assert ridx[:, 0].tolist() == [1, 0] and rv.tolist() == [[3.0], [2.0]]
+    assert kept(rv) == gold["optimum"] and rounds == 1
+
+
+@pytest.mark.parametrize("n,m,g,M,K", LAYOUTS)
+def test_refine_is_a_local_optimum_between_greedy_and_optimum(n, m, g, M, K):
+    rng = np.random.default_rng(11 * M + K)
+    W = rng.standard_normal((M, K)).astype(np.float32)
+    values, index = oracle.p_compress(W, n, m, g)
+    rv, ridx, rounds = oracle.p_refine(W, index, n, m, g)
+    pats = oracle.p_patterns(m, n)
+    P, S, B = len(pats), len(pats) * g, K // m
+    assert rounds < 8 * S
+    dense, mask = oracle.p_densify(rv, ridx, K, n, m, g)      # a valid packing of W
+    assert np.array_equal(dense.view(np.uint8), np.where(mask, W, np.zeros_like(W)).view(np.uint8))
+    for c in range(M // S):
+        for b in range(B):
+            sl = slice(c * S, (c + 1) * S)
+            before, after = kept(values[sl, b * n:(b + 1) * n]), kept(rv[sl, b * n:(b + 1) * n])
+            assert after >= before
+            assert after <= chunk_optimum(W, n, m, g, c, b) * (1 + 1e-12)
+            # no pair swap improves (binary64 sums of the binary32 magnitudes)
+            sc = chunk_scores_f32(W, n, m, g, c, b)
+            pa = np.empty(S, int)
+            pa[ridx[sl, b]] = np.arange(S) // g
+            for r in range(S):
+                for q in range(S):
+                    if pa[r] != pa[q]:
+                        gain = (sc[r, pa[q]] + sc[q, pa[r]]) - (sc[r, pa[r]] + sc[q, pa[q]])
+                        assert gain <= 0
+
+
+def chunk_scores_f32(W, n, m, g, c, b):
+    """The layout's scores: binary32 sums of |w| over each pattern's offsets in
+    ascending order, from +0; returned as binary64."""
+    pats = oracle.p_patterns(m, n)
+    S = len(pats) * g
+    rows = np.abs(W[c * S:(c + 1) * S, b * m:(b + 1) * m].astype(np.float32))
+    out = np.zeros((S, len(pats)), np.float64)
+    for p, offs in enumerate(pats):
+        acc = np.zeros(S, np.float32)
+        for o in offs:
+            acc = (acc + rows[:, o]).astype(np.float32)
+        out[:, p] = acc
+    return out
