@@ -237,6 +237,17 @@ nmg_status nmg_p_layout_init(nmg_p_layout *layout, int32_t M, int32_t K, int32_t
 nmg_status nmg_p_compress(const nmg_p_layout *layout, const void *W, int64_t ldw, void *values,
                           uint8_t *index, hipStream_t stream);
 
+/* The swap search of the paper's GPU converter (Section 5.2), from the
+ * packing `index` already holds (nmg_p_compress's, or any valid one): within a
+ * chunk, blocks with different patterns exchange them when that raises the
+ * magnitude the pair keeps.  The paper lets threads race; here each round
+ * every row takes its best improving partner (the largest gain, sums of the
+ * binary32 magnitudes in binary64, ties to the lower row) and mutual best
+ * partners swap, until no swap improves or 8 * S rounds have run.  Rewrites
+ * index (stored as nmg_p_compress stores it) and values (copied from W). */
+nmg_status nmg_p_refine(const nmg_p_layout *layout, const void *W, int64_t ldw, void *values,
+                        uint8_t *index, hipStream_t stream);
+
 /* Y = W_s * X for the chunked layout: X K x N (ldx >= N), Y M x N (ldy >= N),
  * element-aligned; binary32 accumulation in ascending column order of each
  * row.  An index that is not a permutation in every chunk column gives

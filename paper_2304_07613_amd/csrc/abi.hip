@@ -230,6 +230,17 @@ nmg_status nmg_p_compress(const nmg_p_layout *L, const void *W, int64_t ldw, voi
     return launch_p_compress(L, W, ldw, values, index, stream);
 }
 
+nmg_status nmg_p_refine(const nmg_p_layout *L, const void *W, int64_t ldw, void *values,
+                        uint8_t *index, hipStream_t stream) {
+    nmg_status st = check_p_layout(L);
+    if (st != NMG_OK) return st;
+    if (!W || !values || !index) return NMG_ERR_NULL;
+    if (ldw < L->K) return NMG_ERR_PARAM;
+    const size_t es = elem_size(L->dtype);
+    if (!aligned(W, es) || !aligned(values, es)) return NMG_ERR_ALIGN;
+    return launch_p_refine(L, W, ldw, values, index, stream);
+}
+
 nmg_status nmg_p_spmm(const nmg_p_layout *L, const void *values, const uint8_t *index,
                       const void *X, int64_t ldx, int64_t N, void *Y, int64_t ldy,
                       hipStream_t stream) {

@@ -17,6 +17,13 @@
 //                 one chunk and 256 tokens, and finds each row's position in
 //                 every block column through an inverse table built in LDS.
 //   k_p_densify   one thread per stored block.
+//   k_p_refine    the swap search of the paper's GPU converter (Section 5.2),
+//                 in a fixed order: one workgroup per chunk, one thread per
+//                 row; each round every row finds its best improving partner
+//                 (binary64 gains of the binary32 magnitudes, ties to the lower
+//                 row) and mutual best partners swap, until no swap improves
+//                 (at most 8 * S rounds).  Gains are symmetric, so while a swap
+//                 improves there is a mutual pair.
 #include "common.hpp"
 
 namespace {
@@ -153,6 +160,81 @@ __global__ __launch_bounds__(kBlock) void k_p_densify(const T *__restrict__ valu
     for (int k = 0; k < n; ++k) o[off[k]] = v[k];
 }
 
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_p_refine(const T *__restrict__ W, int64_t ldw,
+                                                     T *__restrict__ values, uint8_t *__restrict__ index,
+                                                     int n, int m, int g, int P, int S, int B) {
+    using Bt = typename Bits<T>::type;
+    __shared__ float wabs[kPMaxWblk];
+    __shared__ float score[kPMaxPairs];
+    __shared__ uint8_t pat[kPMaxPat];
+    __shared__ int pa[kPMaxS];     // pattern of each chunk row
+    __shared__ int best[kPMaxS];   // best improving partner, or -1
+    __shared__ int any;
+    const int c = blockIdx.x, b = blockIdx.y, t = threadIdx.x;
+    const int64_t row0 = (int64_t)c * S, ldv = (int64_t)B * n;
+
+    for (int i = t; i < S * m; i += kBlock)
+        wabs[i] = p_abs(W + (row0 + i / m) * ldw + (int64_t)b * m + i % m);
+    for (int p = t; p < P; p += kBlock) p_unrank(m, n, p, pat + p * n);
+    // the packing to start from (a malformed index leaves rows on pattern 0
+    // and never reads outside the tables)
+    for (int r = t; r < S; r += kBlock) pa[r] = 0;
+    __syncthreads();
+    for (int j = t; j < S; j += kBlock) pa[min((int)index[(row0 + j) * B + b], S - 1)] = j / g;
+    __syncthreads();
+    for (int i = t; i < S * P; i += kBlock) {
+        const int r = i / P, p = i % P;
+        float s = 0.f;  // binary32, the pattern's offsets ascending, from +0
+        for (int k = 0; k < n; ++k) s = s + wabs[r * m + pat[p * n + k]];
+        score[i] = s;
+    }
+    for (int round = 0; round < 8 * S; ++round) {
+        if (t == 0) any = 0;
+        __syncthreads();  // scores, patterns and the flag are ready
+        for (int r = t; r < S; r += kBlock) {
+            const int a = pa[r];
+            int bq = -1;
+            double bg = 0.0;
+            for (int q = 0; q < S; ++q) {
+                const int e = pa[q];
+                if (e == a) continue;
+                const double gain = ((double)score[r * P + e] + (double)score[q * P + a]) -
+                                    ((double)score[r * P + a] + (double)score[q * P + e]);
+                if (gain > bg) {  // strictly larger: ties keep the lower q
+                    bg = gain;
+                    bq = q;
+                }
+            }
+            best[r] = bq;
+            if (bq >= 0) any = 1;
+        }
+        __syncthreads();
+        if (any == 0) break;  // uniform: read after the barrier
+        for (int r = t; r < S; r += kBlock) {
+            const int q = best[r];
+            if (q > r && best[q] == r) {  // mutual best partners: disjoint pairs
+                const int a = pa[r];
+                pa[r] = pa[q];
+                pa[q] = a;
+            }
+        }
+        __syncthreads();  // the flag is reset only after every thread has read it
+    }
+    __syncthreads();
+
+    // stored like nmg_p_compress's result: patterns in order, rows of a group ascending
+    for (int r = t; r < S; r += kBlock) {
+        const int p = pa[r];
+        int pos = p * g;
+        for (int q = 0; q < r; ++q) pos += pa[q] == p;
+        index[(row0 + pos) * B + b] = (uint8_t)r;
+        for (int k = 0; k < n; ++k)
+            reinterpret_cast<Bt *>(values)[(row0 + pos) * ldv + (int64_t)b * n + k] =
+                reinterpret_cast<const Bt *>(W)[(row0 + r) * ldw + (int64_t)b * m + pat[p * n + k]];
+    }
+}
+
 constexpr int kPMaxWaves = kPMaxS / kPRowsWave;  // 16 waves cover the largest chunk
 
 template <typename T>
@@ -250,6 +332,20 @@ nmg_status launch_p_compress(const nmg_p_layout *L, const void *W, int64_t ldw, 
                            ldw, (float *)values, index, L->n, L->m, L->g, L->P, L->S, L->B);
     else
         hipLaunchKernelGGL((k_p_compress<_Float16>), grid, dim3(kBlock), 0, stream,
+                           (const _Float16 *)W, ldw, (_Float16 *)values, index, L->n, L->m, L->g,
+                           L->P, L->S, L->B);
+    return launched();
+}
+
+nmg_status launch_p_refine(const nmg_p_layout *L, const void *W, int64_t ldw, void *values,
+                           uint8_t *index, hipStream_t stream) {
+    if (!p_fits(L)) return NMG_ERR_UNSUPPORTED;
+    dim3 grid(L->M / L->S, L->B);
+    if (L->dtype == NMG_F32)
+        hipLaunchKernelGGL((k_p_refine<float>), grid, dim3(kBlock), 0, stream, (const float *)W,
+                           ldw, (float *)values, index, L->n, L->m, L->g, L->P, L->S, L->B);
+    else
+        hipLaunchKernelGGL((k_p_refine<_Float16>), grid, dim3(kBlock), 0, stream,
                            (const _Float16 *)W, ldw, (_Float16 *)values, index, L->n, L->m, L->g,
                            L->P, L->S, L->B);
     return launched();

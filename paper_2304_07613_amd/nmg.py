@@ -86,6 +86,7 @@ def lib():
         "nmg_p_layout_init": ([pp, i32, i32, i32, i32, i32, ctypes.c_int], ctypes.c_int),
         "nmg_p_compress": ([pp, vp, i64, vp, vp, vp], ctypes.c_int),
         "nmg_p_spmm": ([pp, vp, vp, vp, i64, i64, vp, i64, vp], ctypes.c_int),
+        "nmg_p_refine": ([pp, vp, i64, vp, vp, vp], ctypes.c_int),
         "nmg_p_densify": ([pp, vp, vp, vp, i64, vp], ctypes.c_int),
         "nmg_status_str": ([ctypes.c_int], ctypes.c_char_p),
         "nmg_version": ([], ctypes.c_char_p),
@@ -364,3 +365,20 @@ def p_densify(values, index, layout: PLayout):
     _check(lib().nmg_p_densify(ctypes.byref(layout.c), _ptr(values), _ptr(index), _ptr(out),
                                layout.K, _stream(values)), "nmg_p_densify")
     return out
+
+
+def p_refine(W: torch.Tensor, index: torch.Tensor, layout: PLayout):
+    """The swap search of Section 5.2's GPU converter from the packing `index`:
+    returns new (values, index); the inputs are not changed."""
+    _need_cuda(W, index)
+    if W.dtype != layout.dtype or index.dtype != torch.uint8:
+        raise TypeError("dtype mismatch")
+    if tuple(W.shape) != (layout.M, layout.K):
+        raise ValueError(f"W must be {layout.M} x {layout.K}")
+    if tuple(index.shape) != layout.index_shape:
+        raise ValueError(f"index must be {layout.index_shape}")
+    idx = index.contiguous().clone()
+    values = torch.empty(layout.values_shape, dtype=W.dtype, device=W.device)
+    _check(lib().nmg_p_refine(ctypes.byref(layout.c), _ptr(W), _rows(W, "W"), _ptr(values),
+                              _ptr(idx), _stream(W)), "nmg_p_refine")
+    return values, idx

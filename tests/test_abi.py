@@ -132,5 +132,7 @@ def test_chunked_layout_validation(lib):
     assert lib.nmg_p_compress(ctypes.byref(L), odd, 16, p, p, s) == nmg.ERR_ALIGN
     assert lib.nmg_p_spmm(ctypes.byref(L), p, p, p, 8, 16, p, 16, s) == nmg.ERR_PARAM  # ldx < N
     assert lib.nmg_p_densify(ctypes.byref(L), p, None, p, 16, s) == nmg.ERR_NULL
+    assert lib.nmg_p_refine(ctypes.byref(L), p, 8, p, p, s) == nmg.ERR_PARAM       # ldw < K
+    assert lib.nmg_p_refine(ctypes.byref(L), p, 16, p, None, s) == nmg.ERR_NULL
     bad = nmg._PLayout(48, 16, 2, 4, 2, 6, 10, 4, nmg.F16)   # S inconsistent with P * g
     assert lib.nmg_p_compress(ctypes.byref(bad), p, 16, p, p, s) == nmg.ERR_PARAM

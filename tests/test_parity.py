@@ -494,3 +494,23 @@ def test_chunked_layout_ffn_shape(nmg):
     Yref = rd[rows].astype(np.float64) @ Xd
     B = np.abs(rd[rows].astype(np.float64)) @ np.abs(Xd)
     check_product(Y[torch.as_tensor(rows, device=Y.device)], Yref, B, torch.float32, "chunked ffn")
+
+
+
+@pytest.mark.parametrize("M,K,N,n,m,g,dtype", P_SHAPES[:6],
+                         ids=[f"{c[0]}x{c[1]}-{c[3]}:{c[4]}:{c[5]}-{str(c[6])[6:]}" for c in P_SHAPES[:6]])
+def test_chunked_swap_search(nmg, M, K, N, n, m, g, dtype):
+    """The swap search from the greedy packing and from the identity packing
+    (every chunk's rows in order), bit-exact against the oracle's."""
+    W = synth.normal((M, K), 91 + M, 0.02, dtype)
+    Wd = W.to(DEV)
+    v, idx, L = nmg.p_compress(Wd, n, m, g)
+    ident = torch.from_numpy(np.tile(np.arange(L.S, dtype=np.uint8), M // L.S)[:, None]
+                             .repeat(L.B, axis=1)).to(DEV)
+    for start, name in ((idx, "greedy"), (ident, "identity")):
+        print(f"[swap] {M}x{K} {n}:{m}:{g} {dtype} from {name}", flush=True)
+        rv_g, ridx_g = nmg.p_refine(Wd, start, L)
+        torch.cuda.synchronize()
+        rv, ridx, rounds = oracle.p_refine(np_of(W), np_of(start), n, m, g)
+        assert np.array_equal(np_of(ridx_g), ridx), name
+        assert np.array_equal(bits(np_of(rv_g)), bits(rv)), name
