@@ -57,6 +57,8 @@ def parse():
     ap.add_argument("--workload", type=int, choices=(1, 2, 3), default=2)
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--stack", action="store_true")
+    ap.add_argument("--chunked", action="store_true",
+                    help="the paper's chunked layout beside the group layout on the sweep shapes")
     ap.add_argument("--copy-calibration", action="store_true")
     ap.add_argument("--rotate-mb", type=float, default=1100.0,
                     help="total size of the rotated buffer sets")
@@ -347,6 +349,51 @@ def sweep(ctx, args):
         del res
 
 
+def chunked(ctx, args):
+    """The paper's chunked layout beside the group layout on the sweep shapes
+    it fits (K % m == 0, M % (C(m,n) * g) == 0): kept magnitude of the group
+    layout, of the chunked layout's greedy and of its swap search; converter
+    and product times (events around `reps` back-to-back launches each)."""
+    torch, nmg, synth = ctx.torch, ctx.nmg, ctx.synth
+    import math
+    reps = max(3, args.steps // 20)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        a, b = ctx.event(), ctx.event()
+        a.record(ctx.stream)
+        for _ in range(reps):
+            fn()
+        b.record(ctx.stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps * 1e3  # us
+
+    for j, lin in enumerate(synth.SWEEP.layers):
+        S = math.comb(lin.m, lin.n) * lin.g
+        if lin.n == lin.m or lin.K % lin.m or lin.M % S or S > 256:
+            continue
+        W, X = synth.layer_inputs(5, j, lin)
+        W, X = W.to(ctx.dev), X.to(ctx.dev)
+        total = float(W.double().abs().sum())
+        v, idx, L = nmg.compress(W, lin.n, lin.m, lin.g)
+        pv, pidx, PL = nmg.p_compress(W, lin.n, lin.m, lin.g)
+        rv, ridx = nmg.p_refine(W, pidx, PL)
+        e = lambda vals: round(float(vals.double().abs().sum()) / total, 5)
+        rec = {"mode": "chunked-vs-group", "point": lin.name, "shape": [lin.M, lin.K, lin.N],
+               "rows_per_chunk": S,
+               "energy_group": e(v), "energy_chunked_greedy": e(pv), "energy_chunked_swap": e(rv),
+               "us_compress_group": round(timed(lambda: nmg.compress(W, lin.n, lin.m, lin.g)), 2),
+               "us_compress_chunked": round(timed(lambda: nmg.p_compress(W, lin.n, lin.m, lin.g)), 2),
+               "us_swap_search": round(timed(lambda: nmg.p_refine(W, pidx, PL)), 2),
+               "us_spmm_group": round(timed(lambda: nmg.spmm(v, idx, X, L)), 2),
+               "us_spmm_chunked": round(timed(lambda: nmg.p_spmm(pv, pidx, X, PL)), 2),
+               "group_kernel": nmg.auto_kernel(L, lin.N)}
+        rec["tflops_spmm_chunked"] = round(lin.useful_flop / rec["us_spmm_chunked"] / 1e6, 2)
+        rec["tflops_spmm_group"] = round(lin.useful_flop / rec["us_spmm_group"] / 1e6, 2)
+        print(json.dumps(rec), flush=True)
+
+
 def stack(ctx, args):
     """Forward of the 12-layer fp16 linear stack (48 sparse products, 12 GELU,
     24 residual sums), weights compressed once beforehand."""
@@ -414,6 +461,8 @@ def main():
         sweep(ctx, args)
     elif args.stack:
         stack(ctx, args)
+    elif args.chunked:
+        chunked(ctx, args)
     else:
         headline(ctx, args)
 
