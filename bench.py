@@ -43,7 +43,8 @@ FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense binary32 matrix peak
 FP32_VALU_PEAK_TFLOPS = 78.6    # binary32 vector FMA without packed math (2 FLOP/lane/clk)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "spmm_bert-ffn-up_traffic.txt")
 KERNEL_SYMBOL = {"mfma_scalar": "k_spmm_mfma_s", "mfma_general": "k_spmm_mfma",
-                 "mfma_f16": "k_spmm_mfma_h", "valu": "k_spmm_valu"}
+                 "mfma_f16": "k_spmm_mfma_h", "mfma_direct": "k_spmm_mfma_d",
+                 "valu": "k_spmm_valu"}
 
 
 def parse():
@@ -52,7 +53,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--kernel", choices=("auto", "mfma", "valu", "mfma_general", "mfma_scalar",
-                                         "mfma_f16"),
+                                         "mfma_f16", "mfma_direct"),
                     default="auto")
     ap.add_argument("--workload", type=int, choices=(1, 2, 3), default=2)
     ap.add_argument("--sweep", action="store_true")
@@ -206,7 +207,7 @@ def family_times(ctx, L, sets, kernel, reps=20):
     the timed region): the evidence behind the automatic choice."""
     torch, nmg = ctx.torch, ctx.nmg
     out = {}
-    for fam in ("mfma_f16", "mfma_scalar", "mfma_general", "valu"):
+    for fam in ("mfma_f16", "mfma_direct", "mfma_scalar", "mfma_general", "valu"):
         try:
             for r in range(3):
                 W, X, v, idx, Y = sets[r % len(sets)]

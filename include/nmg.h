@@ -93,13 +93,20 @@ typedef enum nmg_kernel {
                                     window moved to scalar registers and wider
                                     token tiles; additionally needs n a power of
                                     two and a window of 4..16 k-slots          */
-    NMG_KERNEL_MFMA_F16 = 5      /* binary16 layouts on the binary16 matrix
+    NMG_KERNEL_MFMA_F16 = 5,     /* binary16 layouts on the binary16 matrix
                                     cores, 4 k-slots per instruction (binary32
                                     accumulation); needs g % 4 == 0, n a power
                                     of two, the chunks of max(4, n) k-slots
                                     within 512 staged X rows (m <= 128 for
                                     n <= 4), X and ldx on 16-byte boundaries
                                     and N % 8 == 0                            */
+    NMG_KERNEL_MFMA_DIRECT = 6   /* binary32 matrix cores fed by gathering each
+                                    group's selected X rows straight from
+                                    global memory (no staging of whole
+                                    windows), with the k-slots split over the
+                                    waves of a workgroup when the layer alone
+                                    cannot fill the GPU; needs g % 4 == 0 and
+                                    n a power of two                          */
 } nmg_kernel;
 /* With n == m every column is kept and every index row is 0 .. m-1, so the
  * matrix-core kernels treat the weight as one group whatever g is. */

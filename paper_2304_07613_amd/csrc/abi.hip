@@ -109,6 +109,7 @@ nmg_kernel nmg_spmm_auto_kernel(const nmg_layout *L, int64_t N) {
         L = &dense;
     }
     if (spmm_half_supported(L, nullptr, N, N)) return NMG_KERNEL_MFMA_F16;
+    if (spmm_direct_preferred(L, N)) return NMG_KERNEL_MFMA_DIRECT;
     if (spmm_scalar_supported(L, nullptr, N)) return NMG_KERNEL_MFMA_SCALAR;
     return spmm_general_supported(L, N) ? NMG_KERNEL_MFMA_GENERAL : NMG_KERNEL_VALU;
 }
@@ -153,13 +154,14 @@ nmg_status nmg_spmm_epilogue(const nmg_layout *L, nmg_kernel kernel, nmg_epilogu
     SpmmArgs a{L, values, indices, X, ldx, (int)N, Y, ldy, stream};
     const bool half_ok = spmm_half_supported(L, X, ldx, N);
     const bool scalar_ok = spmm_scalar_supported(L, indices, ldx);
-    if (kernel == NMG_KERNEL_AUTO) {
-        kernel = half_ok                          ? NMG_KERNEL_MFMA_F16
-                 : scalar_ok                      ? NMG_KERNEL_MFMA_SCALAR
-                 : spmm_general_supported(L, N) ? NMG_KERNEL_MFMA_GENERAL
-                                                  : NMG_KERNEL_VALU;
-    } else if (kernel == NMG_KERNEL_MFMA) {
-        kernel = half_ok ? NMG_KERNEL_MFMA_F16 : scalar_ok ? NMG_KERNEL_MFMA_SCALAR : NMG_KERNEL_MFMA_GENERAL;
+    if (kernel == NMG_KERNEL_AUTO || kernel == NMG_KERNEL_MFMA) {
+        const bool direct = spmm_direct_preferred(L, N) && spmm_direct_supported(L, ldx);
+        kernel = half_ok     ? NMG_KERNEL_MFMA_F16
+                 : direct    ? NMG_KERNEL_MFMA_DIRECT
+                 : scalar_ok ? NMG_KERNEL_MFMA_SCALAR
+                 : spmm_general_supported(L, N) || kernel == NMG_KERNEL_MFMA
+                     ? NMG_KERNEL_MFMA_GENERAL
+                     : NMG_KERNEL_VALU;
     }
     switch (kernel) {
         case NMG_KERNEL_MFMA_F16:
@@ -168,6 +170,10 @@ nmg_status nmg_spmm_epilogue(const nmg_layout *L, nmg_kernel kernel, nmg_epilogu
             a.R = R;
             a.ldr = ldr;
             return spmm_half(a);
+        case NMG_KERNEL_MFMA_DIRECT:
+            if (!spmm_direct_supported(L, ldx)) return NMG_ERR_UNSUPPORTED;
+            st = spmm_direct(a);
+            break;
         case NMG_KERNEL_MFMA_SCALAR:
             if (!scalar_ok) return NMG_ERR_UNSUPPORTED;
             st = spmm_scalar(a);

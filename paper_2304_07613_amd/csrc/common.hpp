@@ -96,6 +96,10 @@ nmg_status spmm_scalar_f32_u8(const SpmmArgs &a);
 nmg_status spmm_scalar_f32_u4(const SpmmArgs &a);
 nmg_status spmm_scalar_f16(const SpmmArgs &a);
 
+bool spmm_direct_supported(const nmg_layout *L, int64_t ldx);
+bool spmm_direct_preferred(const nmg_layout *L, int64_t N);
+nmg_status spmm_direct(const SpmmArgs &a);
+
 bool spmm_half_supported(const nmg_layout *L, const void *X, int64_t ldx, int64_t N);
 
 nmg_status check_p_layout(const nmg_p_layout *L);

@@ -74,12 +74,19 @@ def test_calls_reject_bad_arguments_before_launch(lib):
     assert lib.nmg_compress(ctypes.byref(bad), p, 64, p, p, s) == nmg.ERR_PARAM
     # g % 4 != 0: the matrix-core kernel declines, the vector kernel is the choice
     assert lib.nmg_layout_init(ctypes.byref(L), 64, 64, 1, 4, 2, nmg.F32) == nmg.OK
-    for fam in ("mfma", "mfma_general", "mfma_scalar", "mfma_f16"):
+    for fam in ("mfma", "mfma_general", "mfma_scalar", "mfma_f16", "mfma_direct"):
         assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS[fam], p, p, p, 32, 32, p, 32,
                                  s) == nmg.ERR_UNSUPPORTED
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 32) == nmg.KERNELS["valu"]
     assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 1, 4, 8, nmg.F32) == nmg.OK
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_scalar"]
+    # 1:10 with groups of 16: gathering the selected rows reads less than
+    # staging whole windows
+    assert lib.nmg_layout_init(ctypes.byref(L), 768, 3072, 1, 10, 16, nmg.F32) == nmg.OK
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_direct"]
+    # a layer too small to fill the GPU without splitting its k-slots
+    assert lib.nmg_layout_init(ctypes.byref(L), 768, 768, 2, 4, 4, nmg.F32) == nmg.OK
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 128) == nmg.KERNELS["mfma_direct"]
     # n = 3 is not a power of two: the general matrix-core kernel declines too
     assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 3, 8, 8, nmg.F32) == nmg.OK
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["valu"]
@@ -100,6 +107,10 @@ def test_calls_reject_bad_arguments_before_launch(lib):
     assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS["mfma_f16"], p, p, p, 32, 32, p, 32,
                              s) == nmg.ERR_UNSUPPORTED
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["valu"]
+    # the gathering kernel is binary32 only
+    assert lib.nmg_layout_init(ctypes.byref(L), 64, 64, 1, 4, 8, nmg.F16) == nmg.OK
+    assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS["mfma_direct"], p, p, p, 32, 32, p, 32,
+                             s) == nmg.ERR_UNSUPPORTED
 
 
 def test_status_strings(lib):

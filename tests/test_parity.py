@@ -81,7 +81,7 @@ def spmm_full(nmg, v, idx, L, X, rv, ridx, kernel, tag=""):
 
 
 # every kernel family; the matrix-core ones decline layouts they cannot take
-KERNELS = ["auto", "valu", "mfma_general", "mfma_scalar", "mfma_f16"]
+KERNELS = ["auto", "valu", "mfma_general", "mfma_scalar", "mfma_f16", "mfma_direct"]
 
 
 def kernels_for(nmg, L, N):
@@ -115,6 +115,11 @@ SMALL = [
     (96, 48, 304, 2, 4, 12, torch.float16),     # g = 12
     (64, 40, 8, 4, 4, 1, torch.float16),        # dense control, N = 8
     (128, 84, 40, 1, 20, 32, torch.float16),    # 1:20, windows of 4 k-slots, tail 4
+    # gathering kernel: many windows split unevenly over waves, n above the
+    # window, a last window past the k-slots
+    (272, 3000, 70, 1, 10, 16, torch.float32),
+    (64, 40, 21, 16, 20, 4, torch.float32),     # n = 16 > 8 k-slots per window
+    (1024, 300, 1, 2, 4, 8, torch.float32),     # one token, 150 k-slots
 ]
 
 
