@@ -44,6 +44,7 @@ FP32_VALU_PEAK_TFLOPS = 78.6    # binary32 vector FMA without packed math (2 FLO
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "spmm_bert-ffn-up_traffic.txt")
 KERNEL_SYMBOL = {"mfma_scalar": "k_spmm_mfma_s", "mfma_general": "k_spmm_mfma",
                  "mfma_f16": "k_spmm_mfma_h", "mfma_direct": "k_spmm_mfma_d",
+                 "smfmac_f16": "k_spmm_smfmac",
                  "valu": "k_spmm_valu"}
 
 
@@ -53,7 +54,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--kernel", choices=("auto", "mfma", "valu", "mfma_general", "mfma_scalar",
-                                         "mfma_f16", "mfma_direct"),
+                                         "mfma_f16", "mfma_direct", "smfmac_f16"),
                     default="auto")
     ap.add_argument("--workload", type=int, choices=(1, 2, 3), default=2)
     ap.add_argument("--sweep", action="store_true")
@@ -207,7 +208,7 @@ def family_times(ctx, L, sets, kernel, reps=20):
     the timed region): the evidence behind the automatic choice."""
     torch, nmg = ctx.torch, ctx.nmg
     out = {}
-    for fam in ("mfma_f16", "mfma_direct", "mfma_scalar", "mfma_general", "valu"):
+    for fam in ("smfmac_f16", "mfma_f16", "mfma_direct", "mfma_scalar", "mfma_general", "valu"):
         try:
             for r in range(3):
                 W, X, v, idx, Y = sets[r % len(sets)]

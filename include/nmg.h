@@ -100,13 +100,19 @@ typedef enum nmg_kernel {
                                     within 512 staged X rows (m <= 128 for
                                     n <= 4), X and ldx on 16-byte boundaries
                                     and N % 8 == 0                            */
-    NMG_KERNEL_MFMA_DIRECT = 6   /* binary32 matrix cores fed by gathering each
+    NMG_KERNEL_MFMA_DIRECT = 6,  /* binary32 matrix cores fed by gathering each
                                     group's selected X rows straight from
                                     global memory (no staging of whole
                                     windows), with the k-slots split over the
                                     waves of a workgroup when the layer alone
                                     cannot fill the GPU; needs g % 4 == 0 and
                                     n a power of two                          */
+    NMG_KERNEL_SMFMAC_F16 = 7    /* binary16 layouts on gfx950's sparse matrix
+                                    instruction (2 stored of every aligned 4
+                                    columns): X read as contiguous rows, no
+                                    gather; needs n in {1, 2}, m in {4, 8,
+                                    16}, C * n % 8 == 0, values, indices, X and
+                                    ldx on 16-byte boundaries, N % 8 == 0     */
 } nmg_kernel;
 /* With n == m every column is kept and every index row is 0 .. m-1, so the
  * matrix-core kernels treat the weight as one group whatever g is. */
@@ -167,8 +173,8 @@ typedef enum nmg_epilogue {
 } nmg_epilogue;
 
 /* nmg_spmm_with followed by an epilogue; the result equals nmg_spmm_with
- * followed by nmg_gelu or nmg_add bit for bit.  NMG_KERNEL_MFMA_F16 applies
- * the epilogue in the product kernel (no second pass over Y); the other
+ * followed by nmg_gelu or nmg_add bit for bit.  NMG_KERNEL_MFMA_F16 and
+ * NMG_KERNEL_SMFMAC_F16 apply the epilogue in the product kernel (no second pass over Y); the other
  * families run the elementwise kernel on Y afterwards.  R (ADD only; ignored
  * otherwise, may be NULL) is M x N with leading dimension ldr >= N, the
  * layout's element type, element-aligned, and must not overlap Y. */

@@ -109,6 +109,7 @@ nmg_kernel nmg_spmm_auto_kernel(const nmg_layout *L, int64_t N) {
         L = &dense;
     }
     if (spmm_half_supported(L, nullptr, N, N)) return NMG_KERNEL_MFMA_F16;
+    if (spmm_smfmac_supported(L, nullptr, nullptr, nullptr, N, N)) return NMG_KERNEL_SMFMAC_F16;
     if (spmm_direct_preferred(L, N)) return NMG_KERNEL_MFMA_DIRECT;
     if (spmm_scalar_supported(L, nullptr, N)) return NMG_KERNEL_MFMA_SCALAR;
     return spmm_general_supported(L, N) ? NMG_KERNEL_MFMA_GENERAL : NMG_KERNEL_VALU;
@@ -157,6 +158,7 @@ nmg_status nmg_spmm_epilogue(const nmg_layout *L, nmg_kernel kernel, nmg_epilogu
     if (kernel == NMG_KERNEL_AUTO || kernel == NMG_KERNEL_MFMA) {
         const bool direct = spmm_direct_preferred(L, N) && spmm_direct_supported(L, ldx);
         kernel = half_ok     ? NMG_KERNEL_MFMA_F16
+                 : spmm_smfmac_supported(L, values, indices, X, ldx, N) ? NMG_KERNEL_SMFMAC_F16
                  : direct    ? NMG_KERNEL_MFMA_DIRECT
                  : scalar_ok ? NMG_KERNEL_MFMA_SCALAR
                  : spmm_general_supported(L, N) || kernel == NMG_KERNEL_MFMA
@@ -170,6 +172,12 @@ nmg_status nmg_spmm_epilogue(const nmg_layout *L, nmg_kernel kernel, nmg_epilogu
             a.R = R;
             a.ldr = ldr;
             return spmm_half(a);
+        case NMG_KERNEL_SMFMAC_F16:
+            if (!spmm_smfmac_supported(L, values, indices, X, ldx, N)) return NMG_ERR_UNSUPPORTED;
+            a.epi = epi;  // applied in the product kernel
+            a.R = R;
+            a.ldr = ldr;
+            return spmm_smfmac(a);
         case NMG_KERNEL_MFMA_DIRECT:
             if (!spmm_direct_supported(L, ldx)) return NMG_ERR_UNSUPPORTED;
             st = spmm_direct(a);

@@ -100,6 +100,10 @@ bool spmm_direct_supported(const nmg_layout *L, int64_t ldx);
 bool spmm_direct_preferred(const nmg_layout *L, int64_t N);
 nmg_status spmm_direct(const SpmmArgs &a);
 
+bool spmm_smfmac_supported(const nmg_layout *L, const void *values, const uint8_t *indices,
+                           const void *X, int64_t ldx, int64_t N);
+nmg_status spmm_smfmac(const SpmmArgs &a);
+
 bool spmm_half_supported(const nmg_layout *L, const void *X, int64_t ldx, int64_t N);
 
 nmg_status check_p_layout(const nmg_p_layout *L);

@@ -74,7 +74,7 @@ def test_calls_reject_bad_arguments_before_launch(lib):
     assert lib.nmg_compress(ctypes.byref(bad), p, 64, p, p, s) == nmg.ERR_PARAM
     # g % 4 != 0: the matrix-core kernel declines, the vector kernel is the choice
     assert lib.nmg_layout_init(ctypes.byref(L), 64, 64, 1, 4, 2, nmg.F32) == nmg.OK
-    for fam in ("mfma", "mfma_general", "mfma_scalar", "mfma_f16", "mfma_direct"):
+    for fam in ("mfma", "mfma_general", "mfma_scalar", "mfma_f16", "mfma_direct", "smfmac_f16"):
         assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS[fam], p, p, p, 32, 32, p, 32,
                                  s) == nmg.ERR_UNSUPPORTED
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 32) == nmg.KERNELS["valu"]
@@ -106,7 +106,14 @@ def test_calls_reject_bad_arguments_before_launch(lib):
     assert lib.nmg_layout_init(ctypes.byref(L), 64, 64, 1, 4, 2, nmg.F16) == nmg.OK
     assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS["mfma_f16"], p, p, p, 32, 32, p, 32,
                              s) == nmg.ERR_UNSUPPORTED
-    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["valu"]
+    # g = 2: no quads of rows, but the sparse matrix instruction takes any g
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["smfmac_f16"]
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4100) == nmg.KERNELS["valu"]
+    assert lib.nmg_layout_init(ctypes.byref(L), 64, 96, 1, 3, 2, nmg.F16) == nmg.OK
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["valu"]  # m = 3
+    assert lib.nmg_layout_init(ctypes.byref(L), 64, 40, 2, 8, 1, nmg.F16) == nmg.OK   # C n = 10
+    assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS["smfmac_f16"], p, p, p, 32, 32, p, 32,
+                             s) == nmg.ERR_UNSUPPORTED
     # the gathering kernel is binary32 only
     assert lib.nmg_layout_init(ctypes.byref(L), 64, 64, 1, 4, 8, nmg.F16) == nmg.OK
     assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS["mfma_direct"], p, p, p, 32, 32, p, 32,

@@ -81,7 +81,7 @@ def spmm_full(nmg, v, idx, L, X, rv, ridx, kernel, tag=""):
 
 
 # every kernel family; the matrix-core ones decline layouts they cannot take
-KERNELS = ["auto", "valu", "mfma_general", "mfma_scalar", "mfma_f16", "mfma_direct"]
+KERNELS = ["auto", "valu", "mfma_general", "mfma_scalar", "mfma_f16", "mfma_direct", "smfmac_f16"]
 
 
 def kernels_for(nmg, L, N):
@@ -120,6 +120,15 @@ SMALL = [
     (272, 3000, 70, 1, 10, 16, torch.float32),
     (64, 40, 21, 16, 20, 4, torch.float32),     # n = 16 > 8 k-slots per window
     (1024, 300, 1, 2, 4, 8, torch.float32),     # one token, 150 k-slots
+    # binary16 on the sparse matrix instruction (n <= 2, m in {4, 8, 16},
+    # C * n % 8 == 0): ragged row and token tiles, g = 1, a tail chunk and a
+    # partial last step of 64 columns
+    (200, 256, 136, 2, 8, 1, torch.float16),
+    (72, 192, 24, 1, 4, 2, torch.float16),
+    (128, 92, 64, 2, 8, 8, torch.float16),      # tail chunk of 4, 92 % 64 != 0
+    (16, 128, 8, 1, 16, 16, torch.float16),
+    (512, 256, 512, 2, 4, 4, torch.float16),
+    (32, 1024, 264, 2, 16, 32, torch.float16),
 ]
 
 
