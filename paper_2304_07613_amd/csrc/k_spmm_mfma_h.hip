@@ -17,6 +17,11 @@
 // blocks of the instruction, so one instruction covers 4 rows x 64 tokens x 4
 // k-slots.  A wave covers 64 * TPL tokens: lane l owns tokens l + 64p.
 //
+// With 4 tokens per lane (256-token rows, 512 bytes) the staged rows of odd
+// chunks have the two 64-token halves of each 128 tokens swapped: a
+// transposing read touches 4 rows of 128 bytes, and with n = 1 or 2 they come
+// from chunks of both parities, so two land in each half of the banks.
+//
 // Epilogues (fused, so that Y is written once): GELU looks the rounded
 // product up in the binary16 GELU table, copied into the staging buffers once
 // the last window is done; ADD reads the residual beside the store.  Both
@@ -137,11 +142,23 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
     // are staged but never used for a stored output
     const int copy_sub = lane / LPR;
     const int copy_tok = min(t0 + 8 * (lane % LPR), N - 8);
+    const int copy_tk = 8 * (lane % LPR);
     auto issue_copies = [&](int win, _Float16 *buf) {
         const int ninst = (rpw + RPI - 1) / RPI;
         for (int j = wave; j < ninst; j += nwaves) {
             const int k = min(win * rpw + j * RPI + copy_sub, K - 1);
-            lds_copy16(X + (int64_t)k * ldx + copy_tok, buf + j * RPI * TN);  // K * ldx < 2^31
+            if constexpr (TPL == 4) {
+                // staged rows of odd chunks (counted within the window) swap
+                // the 64-token halves of each 128 tokens, so that a
+                // transposing read of 4 slots from two chunks (n = 1, 2)
+                // puts 2 rows in each half of the LDS banks
+                const int rl = j * RPI + copy_sub;
+                const int par = (rl / m) & 1;
+                const int tok = min(t0 + (copy_tk ^ (par << 6)), N - 8);
+                lds_copy16(X + (int64_t)k * ldx + tok, buf + j * RPI * TN);
+            } else {
+                lds_copy16(X + (int64_t)k * ldx + copy_tok, buf + j * RPI * TN);  // K * ldx < 2^31
+            }
         }
     };
 
@@ -151,6 +168,7 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
     const uint32_t tr_shift = 8 * k_l;                    // its byte of an index word
     const uint32_t tr_chunk = (uint32_t)((k_l >> log2n) * m);  // its slot's chunk within the k-group
     const uint32_t tr_tok = 16 * (lane >> 4) + 4 * (lane & 3);
+    const uint32_t tr_par = (uint32_t)((k_l >> log2n) & 1);
 
     v4f acc[QW][TPL];
 #pragma unroll
@@ -189,10 +207,18 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
             const uint32_t base = (uint32_t)(((4 * kg) >> log2n) * m) + tr_chunk;
             const uint32_t o = min((w[u][kg] >> tr_shift) & 0xffu, (uint32_t)(m - 1));
             const _Float16 *rp = cur + (base + o) * TN + tr_tok;
-            static_for<TPL>([&](auto pc) {
-                constexpr int p = decltype(pc)::value;
-                dst[p] = lds_read_tr(rp + 64 * p);
-            });
+            if constexpr (TPL == 4) {
+                const uint32_t sw = 64u * ((((4 * kg) >> log2n) & 1) ^ tr_par);
+                static_for<TPL>([&](auto pc) {
+                    constexpr int p = decltype(pc)::value;
+                    dst[p] = lds_read_tr(cur + (base + o) * TN + tr_tok + ((64u * p) ^ sw));
+                });
+            } else {
+                static_for<TPL>([&](auto pc) {
+                    constexpr int p = decltype(pc)::value;
+                    dst[p] = lds_read_tr(rp + 64 * p);
+                });
+            }
         };
         read_step(std::integral_constant<int, 0>{}, r[0]);
         static_for<KG * UNITS>([&](auto tc) {

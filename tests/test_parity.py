@@ -129,6 +129,10 @@ SMALL = [
     (16, 128, 8, 1, 16, 16, torch.float16),
     (512, 256, 512, 2, 4, 4, torch.float16),
     (32, 1024, 264, 2, 16, 32, torch.float16),
+    # binary16 with 4 tokens per lane (enough rows x tokens for 8 waves of
+    # 256-token tiles per CU): swizzled staging, a ragged last token tile
+    (2048, 64, 4096, 2, 8, 8, torch.float16),
+    (2048, 72, 4104, 1, 4, 16, torch.float16),
 ]
 
 
