@@ -44,7 +44,7 @@ FP32_VALU_PEAK_TFLOPS = 78.6    # binary32 vector FMA without packed math (2 FLO
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "spmm_bert-ffn-up_traffic.txt")
 KERNEL_SYMBOL = {"mfma_scalar": "k_spmm_mfma_s", "mfma_general": "k_spmm_mfma",
                  "mfma_f16": "k_spmm_mfma_h", "mfma_direct": "k_spmm_mfma_d",
-                 "smfmac_f16": "k_spmm_smfmac",
+                 "smfmac_f16": "k_spmm_smfmac", "valu_staged": "k_spmm_valu_s",
                  "valu": "k_spmm_valu"}
 
 
@@ -54,7 +54,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--kernel", choices=("auto", "mfma", "valu", "mfma_general", "mfma_scalar",
-                                         "mfma_f16", "mfma_direct", "smfmac_f16"),
+                                         "mfma_f16", "mfma_direct", "smfmac_f16",
+                                         "valu_staged"),
                     default="auto")
     ap.add_argument("--workload", type=int, choices=(1, 2, 3), default=2)
     ap.add_argument("--sweep", action="store_true")
@@ -208,7 +209,8 @@ def family_times(ctx, L, sets, kernel, reps=20):
     the timed region): the evidence behind the automatic choice."""
     torch, nmg = ctx.torch, ctx.nmg
     out = {}
-    for fam in ("smfmac_f16", "mfma_f16", "mfma_direct", "mfma_scalar", "mfma_general", "valu"):
+    for fam in ("smfmac_f16", "mfma_f16", "mfma_direct", "mfma_scalar", "mfma_general",
+                "valu_staged", "valu"):
         try:
             for r in range(3):
                 W, X, v, idx, Y = sets[r % len(sets)]

@@ -107,12 +107,17 @@ typedef enum nmg_kernel {
                                     waves of a workgroup when the layer alone
                                     cannot fill the GPU; needs g % 4 == 0 and
                                     n a power of two                          */
-    NMG_KERNEL_SMFMAC_F16 = 7    /* binary16 layouts on gfx950's sparse matrix
+    NMG_KERNEL_SMFMAC_F16 = 7,   /* binary16 layouts on gfx950's sparse matrix
                                     instruction (2 stored of every aligned 4
                                     columns): X read as contiguous rows, no
                                     gather; needs n in {1, 2}, m in {4, 8,
                                     16}, C * n % 8 == 0, values, indices, X and
                                     ldx on 16-byte boundaries, N % 8 == 0     */
+    NMG_KERNEL_VALU_STAGED = 8   /* vector-ALU FMA on X windows staged in LDS
+                                    (the choice for binary32 layouts the
+                                    matrix-core kernels decline, g = 1 above
+                                    all); needs binary32, m <= 32, n <= 16, X
+                                    and ldx on 16-byte boundaries, N % 4 == 0 */
 } nmg_kernel;
 /* With n == m every column is kept and every index row is 0 .. m-1, so the
  * matrix-core kernels treat the weight as one group whatever g is. */

@@ -112,7 +112,8 @@ nmg_kernel nmg_spmm_auto_kernel(const nmg_layout *L, int64_t N) {
     if (spmm_smfmac_supported(L, nullptr, nullptr, nullptr, N, N)) return NMG_KERNEL_SMFMAC_F16;
     if (spmm_direct_preferred(L, N)) return NMG_KERNEL_MFMA_DIRECT;
     if (spmm_scalar_supported(L, nullptr, N)) return NMG_KERNEL_MFMA_SCALAR;
-    return spmm_general_supported(L, N) ? NMG_KERNEL_MFMA_GENERAL : NMG_KERNEL_VALU;
+    if (spmm_general_supported(L, N)) return NMG_KERNEL_MFMA_GENERAL;
+    return spmm_valu_staged_preferred(L, nullptr, N, N) ? NMG_KERNEL_VALU_STAGED : NMG_KERNEL_VALU;
 }
 
 nmg_status nmg_spmm_with(const nmg_layout *L, nmg_kernel kernel, const void *values,
@@ -163,7 +164,8 @@ nmg_status nmg_spmm_epilogue(const nmg_layout *L, nmg_kernel kernel, nmg_epilogu
                  : scalar_ok ? NMG_KERNEL_MFMA_SCALAR
                  : spmm_general_supported(L, N) || kernel == NMG_KERNEL_MFMA
                      ? NMG_KERNEL_MFMA_GENERAL
-                     : NMG_KERNEL_VALU;
+                 : spmm_valu_staged_preferred(L, X, ldx, N) ? NMG_KERNEL_VALU_STAGED
+                                                              : NMG_KERNEL_VALU;
     }
     switch (kernel) {
         case NMG_KERNEL_MFMA_F16:
@@ -192,6 +194,10 @@ nmg_status nmg_spmm_epilogue(const nmg_layout *L, nmg_kernel kernel, nmg_epilogu
             break;
         case NMG_KERNEL_VALU:
             st = spmm_valu(a);
+            break;
+        case NMG_KERNEL_VALU_STAGED:
+            if (!spmm_valu_staged_supported(L, X, ldx, N)) return NMG_ERR_UNSUPPORTED;
+            st = spmm_valu_staged(a);
             break;
         default:
             return NMG_ERR_PARAM;

@@ -84,6 +84,9 @@ nmg_status launch_add(nmg_dtype dtype, const void *a, const void *b, void *out, 
                       hipStream_t stream);
 
 nmg_status spmm_valu(const SpmmArgs &a);
+bool spmm_valu_staged_supported(const nmg_layout *L, const void *X, int64_t ldx, int64_t N);
+bool spmm_valu_staged_preferred(const nmg_layout *L, const void *X, int64_t ldx, int64_t N);
+nmg_status spmm_valu_staged(const SpmmArgs &a);
 
 bool spmm_general_supported(const nmg_layout *L, int64_t N);
 nmg_status spmm_general_f32(const SpmmArgs &a);

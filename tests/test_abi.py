@@ -72,12 +72,23 @@ def test_calls_reject_bad_arguments_before_launch(lib):
     assert lib.nmg_gelu(nmg.F32, p, p, 0, s) == nmg.OK   # empty input: nothing to launch
     bad = nmg._Layout(64, 64, 1, 4, 8, 17, nmg.F32)    # inconsistent C
     assert lib.nmg_compress(ctypes.byref(bad), p, 64, p, p, s) == nmg.ERR_PARAM
-    # g % 4 != 0: the matrix-core kernel declines, the vector kernel is the choice
+    # g % 4 != 0: the matrix-core kernels decline, a vector kernel is the choice
+    # (the LDS-staged one when X rows can be copied 16 bytes at a time)
     assert lib.nmg_layout_init(ctypes.byref(L), 64, 64, 1, 4, 2, nmg.F32) == nmg.OK
     for fam in ("mfma", "mfma_general", "mfma_scalar", "mfma_f16", "mfma_direct", "smfmac_f16"):
         assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS[fam], p, p, p, 32, 32, p, 32,
                                  s) == nmg.ERR_UNSUPPORTED
-    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 32) == nmg.KERNELS["valu"]
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 32) == nmg.KERNELS["valu_staged"]
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 30) == nmg.KERNELS["valu"]    # N % 4 != 0
+    assert lib.nmg_layout_init(ctypes.byref(L), 64, 660, 1, 33, 1, nmg.F32) == nmg.OK
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 32) == nmg.KERNELS["valu"]    # m > 32
+    assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS["valu_staged"], p, p, p, 32, 32, p, 32,
+                             s) == nmg.ERR_UNSUPPORTED
+    # 1:20, g = 1: a window of one k-slot, the gathering vector kernel is faster
+    assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 1, 20, 1, nmg.F32) == nmg.OK
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["valu"]
+    assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 1, 10, 1, nmg.F32) == nmg.OK
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["valu_staged"]
     assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 1, 4, 8, nmg.F32) == nmg.OK
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_scalar"]
     # 1:10 with groups of 16: gathering the selected rows reads less than
@@ -89,7 +100,7 @@ def test_calls_reject_bad_arguments_before_launch(lib):
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 128) == nmg.KERNELS["mfma_direct"]
     # n = 3 is not a power of two: the general matrix-core kernel declines too
     assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 3, 8, 8, nmg.F32) == nmg.OK
-    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["valu"]
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["valu_staged"]
     # n = m (dense) with g = 1: one group, so the matrix cores take it
     assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 4, 4, 1, nmg.F32) == nmg.OK
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_scalar"]

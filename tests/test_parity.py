@@ -81,7 +81,8 @@ def spmm_full(nmg, v, idx, L, X, rv, ridx, kernel, tag=""):
 
 
 # every kernel family; the matrix-core ones decline layouts they cannot take
-KERNELS = ["auto", "valu", "mfma_general", "mfma_scalar", "mfma_f16", "mfma_direct", "smfmac_f16"]
+KERNELS = ["auto", "valu", "mfma_general", "mfma_scalar", "mfma_f16", "mfma_direct", "smfmac_f16",
+           "valu_staged"]
 
 
 def kernels_for(nmg, L, N):
@@ -129,6 +130,12 @@ SMALL = [
     (16, 128, 8, 1, 16, 16, torch.float16),
     (512, 256, 512, 2, 4, 4, torch.float16),
     (32, 1024, 264, 2, 16, 32, torch.float16),
+    # the LDS-staged vector kernel: g = 1 and 3, n = 3 and 5, chunks of 32,
+    # ragged rows and tokens, a last window past the chunks
+    (200, 256, 516, 1, 4, 1, torch.float32),
+    (96, 100, 260, 3, 8, 3, torch.float32),
+    (70, 90, 64, 5, 32, 1, torch.float32),
+    (64, 770, 1028, 2, 10, 2, torch.float32),
     # binary16 with 4 tokens per lane (enough rows x tokens for 8 waves of
     # 256-token tiles per CU): swizzled staging, a ragged last token tile
     (2048, 64, 4096, 2, 8, 8, torch.float16),
