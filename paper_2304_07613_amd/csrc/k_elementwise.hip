@@ -88,11 +88,13 @@ __global__ __launch_bounds__(kBlock) void k_compress(
 
 // For m <= MT (MT = 4, 8, 16 or 32): one thread owns one (group, chunk).  It
 // reads the chunk's m columns down the g rows (one vector load per row when
-// the chunk starts on a 16-byte boundary), sums the scores in binary32 in row
-// order, ranks them in registers (the same order as k_compress: key bits,
-// ties to the lower offset), and writes the indices and the kept weights of
-// the g rows.  Adjacent threads own adjacent chunks, so every load and store
-// is coalesced across the wave, and W is read exactly once.
+// the chunk starts on a 16-byte boundary, 4 rows in flight at a time), sums
+// the scores in binary32 in row order, selects the n largest in registers
+// (the same order as k_compress: key bits, ties to the lower offset; n passes
+// of the first maximum for n <= 4, counted ranks otherwise), and writes the
+// indices and the kept weights of the g rows.  Adjacent threads own adjacent
+// chunks, so every load and store is coalesced across the wave, and W is read
+// exactly once.
 template <typename T, int MT>
 __global__ __launch_bounds__(kBlock) void k_compress_chunk(
     const T *__restrict__ W, int64_t ldw, T *__restrict__ values,
@@ -110,26 +112,45 @@ __global__ __launch_bounds__(kBlock) void k_compress_chunk(
     float score[MT];
 #pragma unroll
     for (int j = 0; j < MT; ++j) score[j] = 0.0f;
-    for (int i = 0; i < g; ++i) {
-        const T *p = W + (row0 + i) * ldw + col0;
-        if (vec && w == m) {
-            // m % VB == 0 here: whole 16-byte vectors
+    if (vec && w == m) {
+        // m % VB == 0 here: whole 16-byte vectors.  Rows come 4 at a time
+        // (the loads of 4 rows in flight together), added in row order.
+        typedef B BV __attribute__((ext_vector_type(VB)));
+        constexpr int NV = MT / VB + (MT % VB != 0);
+        auto load_row = [&](int i, BV (&r)[NV]) {
+            const T *p = W + (row0 + i) * ldw + col0;
 #pragma unroll
-            for (int v = 0; v < MT / VB + (MT % VB != 0); ++v) {
-                if (v * VB < m) {
-                    typedef B BV __attribute__((ext_vector_type(VB)));
-                    const BV bits = *reinterpret_cast<const BV *>(p + v * VB);
+            for (int v = 0; v < NV; ++v)
+                if (v * VB < m) r[v] = *reinterpret_cast<const BV *>(p + v * VB);
+        };
+        auto add_row = [&](const BV (&r)[NV]) {
+#pragma unroll
+            for (int v = 0; v < NV; ++v)
+                if (v * VB < m)
 #pragma unroll
                     for (int e = 0; e < VB; ++e) {
                         const int j = v * VB + e;
-                        if (j < MT) {
-                            const B be = bits[e];
-                            score[j] = score[j] + fabsf((float)__builtin_bit_cast(T, be));
-                        }
+                        if (j < MT) score[j] = score[j] + fabsf((float)__builtin_bit_cast(T, (B)r[v][e]));
                     }
-                }
-            }
-        } else {
+        };
+        // 4 rows per batch: their loads in flight together
+        constexpr int RB = 4;
+        int i = 0;
+        for (; i + RB <= g; i += RB) {
+            BV r[RB][NV];
+#pragma unroll
+            for (int b = 0; b < RB; ++b) load_row(i + b, r[b]);
+#pragma unroll
+            for (int b = 0; b < RB; ++b) add_row(r[b]);
+        }
+        for (; i < g; ++i) {
+            BV r0[NV];
+            load_row(i, r0);
+            add_row(r0);
+        }
+    } else {
+        for (int i = 0; i < g; ++i) {
+            const T *p = W + (row0 + i) * ldw + col0;
 #pragma unroll
             for (int j = 0; j < MT; ++j)
                 if (j < w) score[j] = score[j] + fabsf((float)p[j]);
@@ -139,28 +160,55 @@ __global__ __launch_bounds__(kBlock) void k_compress_chunk(
     uint32_t key[MT];
 #pragma unroll
     for (int j = 0; j < MT; ++j)
-        key[j] = __builtin_isnan(score[j]) ? 0x7fc00000u : __float_as_uint(score[j]);
-    int slot = 0;
-    uint8_t sel[MT];
+        key[j] = j < w ? (__builtin_isnan(score[j]) ? 0x7fc00000u : __float_as_uint(score[j])) : 0u;
+    // the kept columns as a bit mask
+    uint32_t taken = 0;
+    if (n <= 4) {
+        // n passes of "first maximum among the columns not taken yet" select
+        // the same set as ranking (higher score first, ties to the lower
+        // offset)
 #pragma unroll
-    for (int j = 0; j < MT; ++j) {
-        if (j < w) {
-            int rank = 0;
+        for (int t = 0; t < 4; ++t) {
+            if (t >= n) break;
+            int best = -1;
+            uint32_t bk = 0;
 #pragma unroll
-            for (int i = 0; i < MT; ++i)
-                if (i < w) rank += (key[i] > key[j]) || (i < j && key[i] == key[j]);
-            if (rank < n) {
-                sel[slot < MT ? slot : 0] = (uint8_t)j;
-                ++slot;
+            for (int j = 0; j < MT; ++j) {
+                const bool cand = j < w && !((taken >> j) & 1u);
+                if (cand && (best < 0 || key[j] > bk)) {
+                    best = j;
+                    bk = key[j];
+                }
+            }
+            taken |= 1u << best;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < MT; ++j) {
+            if (j < w) {
+                int rank = 0;
+#pragma unroll
+                for (int i = 0; i < MT; ++i)
+                    if (i < w) rank += (key[i] > key[j]) || (i < j && key[i] == key[j]);
+                if (rank < n) taken |= 1u << j;
             }
         }
     }
+    // the kept offsets in ascending order, then the kept weights of every row
     uint8_t *ip = indices + (int64_t)G * ldv + (int64_t)c * n;
-    for (int s = 0; s < n; ++s) ip[s] = sel[s];
+    uint32_t t = taken;
+    for (int s = 0; s < n; ++s) {
+        ip[s] = (uint8_t)__builtin_ctz(t);
+        t &= t - 1;
+    }
     for (int i = 0; i < g; ++i) {
         const B *src = reinterpret_cast<const B *>(W + (row0 + i) * ldw + col0);
         B *dst = reinterpret_cast<B *>(values + (row0 + i) * ldv) + (int64_t)c * n;
-        for (int s = 0; s < n; ++s) dst[s] = src[sel[s]];
+        uint32_t u = taken;
+        for (int s = 0; s < n; ++s) {
+            dst[s] = src[__builtin_ctz(u)];
+            u &= u - 1;
+        }
     }
 }
 
