@@ -40,7 +40,15 @@ __global__ __launch_bounds__(kBlock) void k_compress(
     if (active) {
         const T *p = W + row0 * ldw + (int64_t)c * m + o;
         float s = 0.0f;
-        for (int i = 0; i < g; ++i) s = s + fabsf((float)p[(int64_t)i * ldw]);
+        int i = 0;
+        for (; i + 8 <= g; i += 8) {   // the loads of 8 rows in flight, added in row order
+            float v[8];
+#pragma unroll
+            for (int b = 0; b < 8; ++b) v[b] = (float)p[(int64_t)(i + b) * ldw];
+#pragma unroll
+            for (int b = 0; b < 8; ++b) s = s + fabsf(v[b]);
+        }
+        for (; i < g; ++i) s = s + fabsf((float)p[(int64_t)i * ldw]);
         // scores are >= +0 or NaN: as unsigned integers the bit patterns of
         // non-negative floats sort like the floats; NaNs become one value
         // above +inf
