@@ -120,11 +120,34 @@ __global__ __launch_bounds__(kBlock) void k_compress_chunk(
     float score[MT];
 #pragma unroll
     for (int j = 0; j < MT; ++j) score[j] = 0.0f;
-    if (vec && w == m) {
+    typedef B BV __attribute__((ext_vector_type(VB)));
+    constexpr int NV = MT / VB + (MT % VB != 0);
+    // Small groups (g rows of whole 16-byte vectors, 16 vectors at most): every
+    // row's chunk is loaded at once and kept in registers, and the kept
+    // weights are picked from there -- one round trip to memory.
+    constexpr int RMAX = 16;
+    const bool whole = vec && w == m;
+    const bool in_regs = whole && g * NV <= RMAX;
+    BV rr[RMAX];
+    if (in_regs) {
+#pragma unroll
+        for (int q = 0; q < RMAX; ++q) {
+            const int i = q / NV, v = q % NV;
+            if (i < g && v * VB < m) rr[q] = *reinterpret_cast<const BV *>(W + (row0 + i) * ldw + col0 + v * VB);
+        }
+#pragma unroll
+        for (int q = 0; q < RMAX; ++q) {   // rows in ascending order
+            const int i = q / NV, v = q % NV;
+            if (i < g && v * VB < m)
+#pragma unroll
+                for (int e = 0; e < VB; ++e) {
+                    const int j = v * VB + e;
+                    if (j < MT) score[j] = score[j] + fabsf((float)__builtin_bit_cast(T, (B)rr[q][e]));
+                }
+        }
+    } else if (whole) {
         // m % VB == 0 here: whole 16-byte vectors.  Rows come 4 at a time
         // (the loads of 4 rows in flight together), added in row order.
-        typedef B BV __attribute__((ext_vector_type(VB)));
-        constexpr int NV = MT / VB + (MT % VB != 0);
         auto load_row = [&](int i, BV (&r)[NV]) {
             const T *p = W + (row0 + i) * ldw + col0;
 #pragma unroll
@@ -208,6 +231,24 @@ __global__ __launch_bounds__(kBlock) void k_compress_chunk(
     for (int s = 0; s < n; ++s) {
         ip[s] = (uint8_t)__builtin_ctz(t);
         t &= t - 1;
+    }
+    if (in_regs) {
+#pragma unroll
+        for (int i = 0; i < RMAX / NV; ++i) {
+            if (i >= g) continue;
+            B *dst = reinterpret_cast<B *>(values + (row0 + i) * ldv) + (int64_t)c * n;
+            uint32_t u = taken;
+            for (int s = 0; s < n; ++s) {
+                const int j = __builtin_ctz(u);
+                u &= u - 1;
+                B x = 0;
+#pragma unroll
+                for (int jj = 0; jj < MT; ++jj)
+                    if (jj == j) x = (B)rr[i * NV + jj / VB][jj % VB];
+                dst[s] = x;
+            }
+        }
+        return;
     }
     for (int i = 0; i < g; ++i) {
         const B *src = reinterpret_cast<const B *>(W + (row0 + i) * ldw + col0);

@@ -57,12 +57,15 @@ __device__ __forceinline__ h4 lds_read_tr(const _Float16 *p) {
 #endif
 }
 
-template <int U, int KSW, int TPL>
+// AVEC: values rows start on 8-byte and index rows on 4-byte boundaries
+// (ldv % 4 == 0, aligned bases), so a lane loads its 4 weights and an index
+// word with one load each.
+template <int U, int KSW, int TPL, bool AVEC>
 __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
     const _Float16 *__restrict__ values, const uint8_t *__restrict__ indices,
     const _Float16 *__restrict__ X, int64_t ldx, _Float16 *__restrict__ Y, int64_t ldy,
     const _Float16 *__restrict__ R, int64_t ldr, int M, int K, int N, int log2n, int m, int g,
-    int C, int row_tiles, int tiles, int epi, bool avec) {
+    int C, int row_tiles, int tiles, int epi) {
     static_assert(KSW % 4 == 0 && KSW <= 64 && U % 4 == 0 && U <= kHalfRowsWave, "k-groups of 4 slots");
     constexpr int QW = kHalfRowsWave / 4;   // quads per wave
     constexpr int UNITS = kHalfRowsWave / U;
@@ -89,7 +92,6 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
     const int cpw = KSW >> log2n;           // chunks per window
     const int rpw = cpw * m;                // X rows per window (<= half_window_rows(TPL))
     const int nwin = (C + cpw - 1) / cpw;
-    const bool ragged = nwin * KSW > ldv;   // the last window runs past the k-slots
 
     // index row of each unit (rows past M read the last group; never stored)
     const uint8_t *irow[UNITS];
@@ -103,20 +105,31 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
     int aoff[QW];
 #pragma unroll
     for (int q = 0; q < QW; ++q) aoff[q] = min(r0 + 4 * q + (lane & 3), M - 1) * ldv + a_slot;
-    auto load_a = [&](int win, h4 (&a)[QW], bool guarded) {
-        const _Float16 *vb = values + win * KSW;
+    // Every load is unconditional, its slot clamped into the row, and what
+    // is loaded is used only in the window that needs it (slots past the row
+    // get weight 0 there): a branch around a load, or an operation on its
+    // result right after it, would make the compiler wait for every load in
+    // flight -- the next window's copies included -- at that point.  (Not
+    // so for unaligned rows, AVEC false: their elements are combined as they
+    // arrive, which keeps the registers within the budget.)
+    auto load_a = [&](int win, h4 (&a)[QW]) {
+        const int s0 = win * KSW + a_slot;      // first of this lane's 4 slots
 #pragma unroll
         for (int q = 0; q < QW; ++q) {
-            if (avec && !guarded) {
-                a[q] = *reinterpret_cast<const h4 *>(vb + aoff[q]);
+            const _Float16 *vr = values + (aoff[q] - a_slot);   // the row
+            if constexpr (AVEC) {
+                a[q] = *reinterpret_cast<const h4 *>(vr + min(s0, ldv - 4));
             } else {
-                h4 v;
 #pragma unroll
-                for (int k = 0; k < 4; ++k)
-                    v[k] = win * KSW + a_slot + k < ldv ? vb[aoff[q] + k] : (_Float16)0.f;
-                a[q] = v;
+                for (int k = 0; k < 4; ++k) a[q][k] = vr[min(s0 + k, ldv - 1)];
             }
         }
+    };
+    auto use_a = [&](int win, h4 v) {
+        const int s0 = win * KSW + a_slot;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v[k] = s0 + k < ldv ? v[k] : (_Float16)0.f;
+        return v;
     };
     // index words of the window: lane u*IW + j loads word j of unit u
     const int iw_u = min(lane / IW, UNITS - 1), iw_j = lane % IW;
@@ -124,15 +137,16 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
 #pragma unroll
     for (int u = 1; u < UNITS; ++u)
         if (iw_u == u) iw_row = irow[u];
-    auto load_idx = [&](int win, uint32_t &wv, bool guarded) {
-        const uint8_t *p = iw_row + win * KSW + 4 * iw_j;
-        if (!guarded && (reinterpret_cast<uintptr_t>(p) & 3) == 0) {
-            wv = *reinterpret_cast<const uint32_t *>(p);
-        } else {  // the last window, or an index row not on a 4-byte boundary
+    // (slots past the row read a clamped byte: their weight is 0 and every
+    // offset is clamped into its chunk where it is used)
+    auto load_idx = [&](int win, uint32_t &wv) {
+        const int s0 = win * KSW + 4 * iw_j;
+        if constexpr (AVEC) {
+            wv = *reinterpret_cast<const uint32_t *>(iw_row + min(s0, ldv - 4));
+        } else {
             uint32_t x = 0;
 #pragma unroll
-            for (int b = 0; b < 4; ++b)
-                if (win * KSW + 4 * iw_j + b < ldv) x |= (uint32_t)p[b] << (8 * b);
+            for (int b = 0; b < 4; ++b) x |= (uint32_t)iw_row[min(s0 + b, ldv - 1)] << (8 * b);
             wv = x;
         }
     };
@@ -176,26 +190,28 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
 #pragma unroll
         for (int p = 0; p < TPL; ++p) acc[q][p] = v4f{0.f, 0.f, 0.f, 0.f};
 
-    h4 a0[QW], a1[QW];          // weights of even / odd windows
+    h4 a0[QW], a1[QW];          // weights of even / odd windows, as loaded
     uint32_t w0 = 0, w1 = 0;    // index words of even / odd windows (one per lane)
     issue_copies(0, xs0);
-    load_a(0, a0, ragged && nwin == 1);
-    load_idx(0, w0, ragged && nwin == 1);
+    load_a(0, a0);
+    load_idx(0, w0);
 
-    auto step = [&](int win, _Float16 *cur, _Float16 *nxt, const h4 (&a)[QW], uint32_t wv,
+    auto step = [&](int win, _Float16 *cur, _Float16 *nxt, const h4 (&a_raw)[QW], uint32_t wv,
                     h4 (&a_nxt)[QW], uint32_t &wv_nxt) {
         wait_all_memory();  // this wave's copies and loads for `win` have landed
         __syncthreads();    // cur is complete; every wave is done with nxt
+        h4 a[QW];
+#pragma unroll
+        for (int q = 0; q < QW; ++q) a[q] = use_a(win, a_raw[q]);
         uint32_t w[UNITS][IW];
 #pragma unroll
         for (int u = 0; u < UNITS; ++u)
 #pragma unroll
             for (int j = 0; j < IW; ++j) w[u][j] = __builtin_amdgcn_readlane(wv, u * IW + j);
         if (win + 1 < nwin) {
-            const bool last_guarded = ragged && win + 2 == nwin;
             issue_copies(win + 1, nxt);
-            load_a(win + 1, a_nxt, last_guarded);
-            load_idx(win + 1, wv_nxt, last_guarded);
+            load_a(win + 1, a_nxt);
+            load_idx(win + 1, wv_nxt);
         }
 
         // steps t = kg * UNITS + u: the B operands of k-group kg of unit u
@@ -300,10 +316,10 @@ int half_tpl(const nmg_layout *L, int64_t N) {
     return waves4 >= 8 * (int64_t)device_cus() && half_window(L, 4) ? 4 : 1;
 }
 
-template <int U, int KSW, int TPL>
+template <int U, int KSW, int TPL, bool AVEC>
 nmg_status launch_half(const SpmmArgs &a) {
     const nmg_layout *L = a.L;
-    const void *kern = reinterpret_cast<const void *>(&k_spmm_mfma_h<U, KSW, TPL>);
+    const void *kern = reinterpret_cast<const void *>(&k_spmm_mfma_h<U, KSW, TPL, AVEC>);
     // waves per workgroup: the count whose tiles fill whole rounds of the GPU best
     const int cus = device_cus();
     const int tok_tiles = (a.N + 64 * TPL - 1) / (64 * TPL);
@@ -322,34 +338,39 @@ nmg_status launch_half(const SpmmArgs &a) {
     }
     const int row_tiles = (L->M + kHalfRowsWave * best_w - 1) / (kHalfRowsWave * best_w);
     const int tiles = row_tiles * tok_tiles;
-    const int64_t ldv = (int64_t)L->C * L->n;
-    const bool avec = aligned(a.values, 8) && ldv % 4 == 0;
     int log2n = 0;
     while ((1 << log2n) < L->n) ++log2n;
-    hipLaunchKernelGGL((k_spmm_mfma_h<U, KSW, TPL>), dim3(tiles), dim3(64 * best_w), 0, a.stream,
+    hipLaunchKernelGGL((k_spmm_mfma_h<U, KSW, TPL, AVEC>), dim3(tiles), dim3(64 * best_w), 0, a.stream,
                        (const _Float16 *)a.values, a.indices, (const _Float16 *)a.X, a.ldx,
                        (_Float16 *)a.Y, a.ldy, (const _Float16 *)a.R, a.ldr, L->M, L->K, a.N,
-                       log2n, L->m, L->g, L->C, row_tiles, tiles, (int)a.epi, avec);
+                       log2n, L->m, L->g, L->C, row_tiles, tiles, (int)a.epi);
     return launched();
+}
+
+template <int U, int KSW, int TPL>
+nmg_status launch_half_v(const SpmmArgs &a) {
+    const int64_t ldv = (int64_t)a.L->C * a.L->n;
+    const bool avec = aligned(a.values, 8) && aligned(a.indices, 4) && ldv % 4 == 0;
+    return avec ? launch_half<U, KSW, TPL, true>(a) : launch_half<U, KSW, TPL, false>(a);
 }
 
 template <int U>
 nmg_status launch_half_u(const SpmmArgs &a) {
     if (half_tpl(a.L, a.N) == 4) {
         switch (half_window(a.L, 4)) {
-            case 32: return launch_half<U, 32, 4>(a);
-            case 16: return launch_half<U, 16, 4>(a);
-            case 8: return launch_half<U, 8, 4>(a);
-            case 4: return launch_half<U, 4, 4>(a);
+            case 32: return launch_half_v<U, 32, 4>(a);
+            case 16: return launch_half_v<U, 16, 4>(a);
+            case 8: return launch_half_v<U, 8, 4>(a);
+            case 4: return launch_half_v<U, 4, 4>(a);
             default: return NMG_ERR_UNSUPPORTED;
         }
     }
     switch (half_window(a.L, 1)) {
-        case 64: return launch_half<U, 64, 1>(a);
-        case 32: return launch_half<U, 32, 1>(a);
-        case 16: return launch_half<U, 16, 1>(a);
-        case 8: return launch_half<U, 8, 1>(a);
-        case 4: return launch_half<U, 4, 1>(a);
+        case 64: return launch_half_v<U, 64, 1>(a);
+        case 32: return launch_half_v<U, 32, 1>(a);
+        case 16: return launch_half_v<U, 16, 1>(a);
+        case 8: return launch_half_v<U, 8, 1>(a);
+        case 4: return launch_half_v<U, 4, 1>(a);
         default: return NMG_ERR_UNSUPPORTED;
     }
 }
