@@ -140,6 +140,12 @@ SMALL = [
     # 256-token tiles per CU): swizzled staging, a ragged last token tile
     (2048, 64, 4096, 2, 8, 8, torch.float16),
     (2048, 72, 4104, 1, 4, 16, torch.float16),
+    (2048, 64, 4096, 4, 8, 8, torch.float16),   # n = 4: k-groups of one chunk
+    (2048, 36, 4096, 2, 4, 4, torch.float16),   # C * n = 18: unaligned rows, a part-filled chunk block
+    # binary16 staging by chunk class: n above 2, a window past the chunks
+    (128, 96, 136, 4, 8, 8, torch.float16),
+    (64, 128, 72, 8, 16, 4, torch.float16),
+    (96, 200, 264, 2, 8, 8, torch.float16),     # 25 chunks in one window of 32
 ]
 
 
