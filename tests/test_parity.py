@@ -163,6 +163,45 @@ def test_small_shapes(nmg, M, K, N, n, m, g, dtype):
         spmm_full(nmg, v, idx, L, X, rv, ridx, kernel, "small")
 
 
+def random_layouts(count=100, seed=2304):
+    """Seeded random layouts across the whole parameter space the product
+    takes (n and m of every size class, any g, a ragged tail chunk, ragged
+    token counts, both element types), each small enough for the oracle."""
+    rng = np.random.RandomState(seed)
+    out = []
+    while len(out) < count:
+        m = int(rng.choice([1, 2, 3, 4, 5, 6, 8, 10, 12, 16, 20, 24, 32, 40]))
+        n = min(m, int(rng.choice([1, 1, 2, 2, 3, 4, 8, 16])))
+        g = int(rng.choice([1, 2, 3, 4, 8, 12, 16, 32]))
+        C = int(rng.randint(1, 41))
+        r = m if rng.rand() < 0.5 else int(rng.randint(n, m + 1))   # tail width, >= n
+        K = (C - 1) * m + r
+        M = g * int(rng.randint(1, max(2, 512 // g)))
+        dtype = torch.float16 if rng.rand() < 0.5 else torch.float32
+        N = 8 * int(rng.randint(1, 40)) if rng.rand() < 0.6 else int(rng.randint(1, 300))
+        if M * C * n * N > 20_000_000:
+            continue
+        out.append((M, K, N, n, m, g, dtype))
+    return out
+
+
+RANDOM = random_layouts()
+
+
+@pytest.mark.parametrize("M,K,N,n,m,g,dtype", RANDOM,
+                         ids=[f"r{i}-{c[0]}x{c[1]}x{c[2]}-{c[3]}:{c[4]}:{c[5]}-{str(c[6])[6:]}"
+                              for i, c in enumerate(RANDOM)])
+def test_random_layouts(nmg, M, K, N, n, m, g, dtype):
+    W = synth.normal((M, K), 21 + M + 7 * K, 0.02, dtype)
+    X = synth.normal((K, N), 22 + N + 3 * K, 1.0, dtype)
+    v, idx, L, rv, ridx = check_compress(nmg, W, n, m, g, "random")
+    dense = nmg.densify(v, idx, L)
+    rd, _ = oracle.densify(rv, ridx, K, n, m, g)
+    assert np.array_equal(bits(np_of(dense)), bits(rd))
+    for kernel in kernels_for(nmg, L, N):
+        spmm_full(nmg, v, idx, L, X, rv, ridx, kernel, "random")
+
+
 # ------------------------------------------------------ fixed-mask repack
 
 def random_patterns(rng, groups, K, n, m):
