@@ -526,6 +526,52 @@ def test_chunked_layout(nmg, M, K, N, n, m, g, dtype):
     check_product(Y, Yref, B, dtype, "chunked")
 
 
+def random_chunked(count=30, seed=2305):
+    """Seeded random shapes of the chunked layout: K % m == 0, M a multiple
+    of S = C(m, n) * g <= 256, within the kernels' LDS limits (S P <= 8192,
+    S m <= 8192, P n <= 4096; beyond them the library reports
+    NMG_ERR_UNSUPPORTED)."""
+    from math import comb
+    rng = np.random.RandomState(seed)
+    out = []
+    while len(out) < count:
+        m = int(rng.randint(1, 9))
+        n = int(rng.randint(1, m + 1))
+        P = comb(m, n)
+        gs = [g for g in (1, 2, 3, 4, 8, 16, 32, 64)
+              if P * g <= 256 and P * g * P <= 8192 and P * g * m <= 8192 and P * n <= 4096]
+        if not gs:
+            continue
+        g = int(rng.choice(gs))
+        S = P * g
+        M = S * int(rng.randint(1, max(2, 512 // S)))
+        K = m * int(rng.randint(1, 25))
+        N = int(rng.randint(1, 200))
+        dtype = torch.float16 if rng.rand() < 0.5 else torch.float32
+        out.append((M, K, N, n, m, g, dtype))
+    return out
+
+
+P_RANDOM = random_chunked()
+
+
+@pytest.mark.parametrize("M,K,N,n,m,g,dtype", P_RANDOM,
+                         ids=[f"p{i}-{c[0]}x{c[1]}x{c[2]}-{c[3]}:{c[4]}:{c[5]}-{str(c[6])[6:]}"
+                              for i, c in enumerate(P_RANDOM)])
+def test_chunked_random(nmg, M, K, N, n, m, g, dtype):
+    """Converter, densify, product and swap search of the chunked layout on
+    random shapes, against the oracle."""
+    test_chunked_layout(nmg, M, K, N, n, m, g, dtype)
+    W = synth.normal((M, K), 81 + M, 0.02, dtype)
+    Wd = W.to(DEV)
+    v, idx, L = nmg.p_compress(Wd, n, m, g)
+    rv_g, ridx_g = nmg.p_refine(Wd, idx, L)
+    torch.cuda.synchronize()
+    rv, ridx, rounds = oracle.p_refine(np_of(W), np_of(idx), n, m, g)
+    assert np.array_equal(np_of(ridx_g), ridx)
+    assert np.array_equal(bits(np_of(rv_g)), bits(rv))
+
+
 def test_chunked_layout_ties_and_nan(nmg):
     rng = np.random.default_rng(5)
     W = (rng.integers(-3, 4, size=(96, 24)) / 2.0).astype(np.float32)   # many equal magnitudes
