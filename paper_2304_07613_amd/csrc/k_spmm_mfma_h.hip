@@ -153,26 +153,39 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
     // X rows of a window into LDS: lane l copies 16 bytes (8 tokens) of row
     // l / LPR; tokens past N (a ragged last token tile) re-read the row's last
     // 8 tokens (host checked: N % 8 == 0), rows past K the last row -- both
-    // are staged but never used for a stored output
+    // are staged but never used for a stored output.
+    // Staged rows of odd chunks (counted within the window) swap the 64-token
+    // halves of each 128 tokens when TPL == 4, so that a transposing read of
+    // 4 slots from two chunks (n = 1, 2) puts 2 rows in each half of the LDS
+    // banks.  The copies are addressed on the scalar unit where they can be:
+    // a uniform row base plus a per-lane offset fixed for the whole kernel,
+    // one per swap parity; a row's chunk parity comes from a multiply.
     const int copy_sub = lane / LPR;
-    const int copy_tok = min(t0 + 8 * (lane % LPR), N - 8);
     const int copy_tk = 8 * (lane % LPR);
+    // element offsets of this lane from its instruction's first row (K * ldx < 2^31)
+    const int sub_off = copy_sub * (int)ldx;
+    const int lane_x0 = sub_off + min(t0 + copy_tk, N - 8);
+    const int lane_x1 = sub_off + min(t0 + (copy_tk ^ 64), N - 8);
+    // r / m by a multiply, exact for r < 2^16 / m (rows of a window: r <= 128)
+    const uint32_t inv_m = (65536u + (uint32_t)m - 1) / (uint32_t)m;
     auto issue_copies = [&](int win, _Float16 *buf) {
         const int ninst = (rpw + RPI - 1) / RPI;
         for (int j = wave; j < ninst; j += nwaves) {
-            const int k = min(win * rpw + j * RPI + copy_sub, K - 1);
+            const int rb = __builtin_amdgcn_readfirstlane(j * RPI);   // first row in the window
+            const int kb = __builtin_amdgcn_readfirstlane(win * rpw + rb);   // and in X
+            const _Float16 *xb = X + (int64_t)kb * ldx;
+            int lx = lane_x0;
             if constexpr (TPL == 4) {
-                // staged rows of odd chunks (counted within the window) swap
-                // the 64-token halves of each 128 tokens, so that a
-                // transposing read of 4 slots from two chunks (n = 1, 2)
-                // puts 2 rows in each half of the LDS banks
-                const int rl = j * RPI + copy_sub;
-                const int par = (rl / m) & 1;
-                const int tok = min(t0 + (copy_tk ^ (par << 6)), N - 8);
-                lds_copy16(X + (int64_t)k * ldx + tok, buf + j * RPI * TN);
-            } else {
-                lds_copy16(X + (int64_t)k * ldx + copy_tok, buf + j * RPI * TN);  // K * ldx < 2^31
+                // RPI == 2: the chunk parities of rows rb and rb + 1
+                const int p0 = __builtin_amdgcn_readfirstlane((int)(((uint32_t)rb * inv_m) >> 16) & 1);
+                const int p1 = __builtin_amdgcn_readfirstlane((int)(((uint32_t)(rb + 1) * inv_m) >> 16) & 1);
+                lx = (copy_sub ? p1 : p0) ? lane_x1 : lane_x0;
             }
+            // rows past K (the last window) read the last row, never selected
+            const int lim = K - kb;
+            const int clamp = __builtin_amdgcn_readfirstlane((lim - 1) * (int)ldx);
+            lx = copy_sub < lim ? lx : lx - sub_off + clamp;
+            lds_copy16(xb + lx, buf + rb * TN);
         }
     };
 
