@@ -202,6 +202,54 @@ def test_random_layouts(nmg, M, K, N, n, m, g, dtype):
         spmm_full(nmg, v, idx, L, X, rv, ridx, kernel, "random")
 
 
+def random_large(count=12, seed=2306):
+    """Seeded random layouts at the workloads' scale (the launch shapes small
+    cases never reach: 4 tokens per lane, several rounds of workgroups,
+    k-splits), checked on sampled outputs."""
+    rng = np.random.RandomState(seed)
+    out = []
+    for _ in range(count):
+        n, m = [(2, 4), (1, 4), (2, 8), (1, 10), (1, 20), (4, 8), (1, 2)][rng.randint(7)]
+        g = int(rng.choice([1, 4, 8, 16, 32]))
+        M = g * int(rng.randint(max(1, 512 // g), 3072 // g + 1))
+        K = int(rng.choice([384, 768, 1000, 2048, 3072]))
+        N = int(rng.choice([512, 1024, 2048, 4096, 4104, 3000]))
+        dtype = torch.float16 if rng.rand() < 0.5 else torch.float32
+        out.append((M, K, N, n, m, g, dtype))
+    return out
+
+
+LARGE = random_large()
+
+
+@pytest.mark.parametrize("M,K,N,n,m,g,dtype", LARGE,
+                         ids=[f"L{i}-{c[0]}x{c[1]}x{c[2]}-{c[3]}:{c[4]}:{c[5]}-{str(c[6])[6:]}"
+                              for i, c in enumerate(LARGE)])
+def test_random_large(nmg, M, K, N, n, m, g, dtype):
+    """Compress compared in full; every kernel family's product on 30000
+    sampled outputs (every token tile and row tile hit) against the oracle."""
+    W = synth.normal((M, K), 31 + M + K, 0.02, dtype)
+    X = synth.normal((K, N), 32 + N, 1.0, dtype)
+    v, idx, L, rv, ridx = check_compress(nmg, W, n, m, g, "large")
+    rng = np.random.RandomState(M * 7 + N)
+    rows = rng.randint(0, M, 30000)
+    cols = rng.randint(0, N, 30000)
+    Yref, B = oracle.spmm_points(rv, ridx, np_of(X), K, n, m, g, rows, cols)
+    Xd = X.to(DEV)
+    for kernel in kernels_for(nmg, L, N):
+        print(f"[spmm] large {L} N={N} kernel={kernel}", flush=True)
+        try:
+            Y = nmg.spmm(v, idx, Xd, L, kernel)
+        except nmg.NmgError as e:
+            if e.status == nmg.ERR_UNSUPPORTED and kernel not in ("auto", "valu"):
+                continue
+            raise
+        torch.cuda.synchronize()
+        Yg = np_of(Y)[rows, cols].astype(np.float64)
+        bad = np.abs(Yg - Yref) > TOL[dtype] * B
+        assert not bad.any(), f"{kernel}: {bad.sum()} sampled outputs out of bound"
+
+
 # ------------------------------------------------------ fixed-mask repack
 
 def random_patterns(rng, groups, K, n, m):
