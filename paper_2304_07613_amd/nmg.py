@@ -153,9 +153,17 @@ def _ptr(t: torch.Tensor):
 
 
 def _need_cuda(*ts):
+    """Every tensor on the current GPU: the library launches on the current
+    HIP device, on that device's current stream."""
+    cur = None
     for t in ts:
         if not t.is_cuda:
             raise ValueError("libnmg works on GPU tensors only")
+        if cur is None:
+            cur = torch.cuda.current_device()
+        if t.device.index != cur:
+            raise ValueError(f"tensor on {t.device}, but the current device is cuda:{cur} "
+                             "(select it with torch.cuda.device)")
 
 
 def _rows(t: torch.Tensor, name: str):
