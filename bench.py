@@ -23,8 +23,9 @@ every kernel would themselves add several microseconds of idle per launch).
 
 Other modes (not the headline): --workload 1|3 (the other single layers),
 --sweep (the n:m x g sweep, one line per point), --stack (the 12-layer fp16
-BERT-base linear stack), --copy-calibration (a plain device copy of known
-size, for scaling the HBM byte counters).
+BERT-base linear stack), --stack-layer 0..3 (one of its projections alone,
+like --workload), --copy-calibration (a plain device copy of known size, for
+scaling the HBM byte counters).
 """
 from __future__ import annotations
 
@@ -44,6 +45,7 @@ METRIC = "nmg_spmm useful GFLOP/s + % HBM roofline, BERT-base FFN 3072x768 @ 75%
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, GB/s
 FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense binary32 matrix peak
 FP32_VALU_PEAK_TFLOPS = 78.6    # binary32 vector FMA without packed math (2 FLOP/lane/clk)
+FP16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense binary16 matrix peak
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "spmm_bert-ffn-up_traffic.txt")
 KERNEL_SYMBOL = {"mfma_scalar": "k_spmm_mfma_s", "mfma_general": "k_spmm_mfma",
                  "mfma_f16": "k_spmm_mfma_h", "mfma_direct": "k_spmm_mfma_d",
@@ -63,6 +65,9 @@ def parse():
     ap.add_argument("--workload", type=int, choices=(1, 2, 3), default=2)
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--stack", action="store_true")
+    ap.add_argument("--stack-layer", type=int, choices=(0, 1, 2, 3), default=None,
+                    help="one projection of the fp16 stack (QKV, attention-out, FFN up, FFN down) "
+                         "timed like --workload, with the other kernel families")
     ap.add_argument("--chunked", action="store_true",
                     help="the paper's chunked layout beside the group layout on the sweep shapes")
     ap.add_argument("--copy-calibration", action="store_true")
@@ -239,9 +244,13 @@ def layer_record(lin, res):
     kernel = res["kernel"]
     spmm_s = res["spmm_ms"] * 1e-3
     tflops = lin.useful_flop / spmm_s / 1e12
-    matrix = kernel.startswith("mfma")
-    # binary32 matrix cores for both input types; the vector kernel without packed math
-    peak = FP32_MFMA_PEAK_TFLOPS if matrix else FP32_VALU_PEAK_TFLOPS
+    matrix = kernel.startswith("mfma") or kernel.startswith("smfmac")
+    # binary16 kernels on the binary16 matrix instructions; the others on the
+    # binary32 ones; the vector kernels without packed math
+    if kernel in ("mfma_f16", "smfmac_f16"):
+        peak = FP16_MFMA_PEAK_TFLOPS
+    else:
+        peak = FP32_MFMA_PEAK_TFLOPS if matrix else FP32_VALU_PEAK_TFLOPS
     rec = {
         "roofline": {
             "kernel": KERNEL_SYMBOL.get(kernel, kernel),
@@ -313,14 +322,15 @@ def cpu_baseline(args, lin, L, set0):
 
 
 def headline(ctx, args):
-    wl = ctx.synth.WORKLOADS[args.workload]
-    lin = wl.layers[0]
-    res = time_layer(ctx, args, args.workload, 0, lin, args.kernel)
+    workload, layer = (4, args.stack_layer) if args.stack_layer is not None else (args.workload, 0)
+    wl = ctx.synth.WORKLOADS[workload]
+    lin = wl.layers[layer]
+    res = time_layer(ctx, args, workload, layer, lin, args.kernel)
     rec = layer_record(lin, res)
-    if args.workload == 2:
+    if workload == 2:
         rec["roofline"]["traffic"] = stored_traffic(traffic_digest())
     out = {
-        "metric": METRIC if args.workload == 2 else "nmg_spmm useful GFLOP/s",
+        "metric": METRIC if workload == 2 else "nmg_spmm useful GFLOP/s",
         "value": round(lin.useful_flop / (res["ms_step"] * 1e-3) / 1e9, 1),
         "unit": "GFLOP/s",
         "n_gpus": 1,
@@ -332,8 +342,9 @@ def headline(ctx, args):
         "vs_baseline": None,
         "dtype": "f32" if lin.dtype.itemsize == 4 else "f16",
         "data": "synthetic",
-        "config": {"workload": wl.key, "M": lin.M, "K": lin.K, "N": lin.N, "n": lin.n,
-                   "m": lin.m, "g": lin.g, "kernel": res["kernel"],
+        "config": {"workload": wl.key if workload != 4 else f"{wl.key}:{lin.name}",
+                   "M": lin.M, "K": lin.K, "N": lin.N, "n": lin.n, "m": lin.m, "g": lin.g,
+                   "kernel": res["kernel"],
                    "rotated_sets": res["n_sets"], "step": "nmg_compress + nmg_spmm"},
         **rec,
         "wall_s_timed": round(res["wall"], 4),
