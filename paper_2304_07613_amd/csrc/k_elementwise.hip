@@ -145,6 +145,9 @@ __global__ __launch_bounds__(kBlock) void k_compress_chunk(
                     if (j < MT) score[j] = score[j] + fabsf((float)__builtin_bit_cast(T, (B)rr[q][e]));
                 }
         }
+        // every row has landed (the scores needed them): said explicitly, so
+        // that the stores below are not each preceded by a wait for memory
+        wait_all_memory();
     } else if (whole) {
         // m % VB == 0 here: whole 16-byte vectors.  Rows come 4 at a time
         // (the loads of 4 rows in flight together), added in row order.
@@ -233,18 +236,26 @@ __global__ __launch_bounds__(kBlock) void k_compress_chunk(
         t &= t - 1;
     }
     if (in_regs) {
+        // the kept offsets in ascending order (slots s < n), then every row's
+        // stores from straight-line code, so that they issue back to back
+        int js[MT];
+        uint32_t u = taken;
+#pragma unroll
+        for (int s = 0; s < MT; ++s) {
+            js[s] = u ? __builtin_ctz(u) : 0;
+            u &= u - 1;
+        }
 #pragma unroll
         for (int i = 0; i < RMAX / NV; ++i) {
             if (i >= g) continue;
             B *dst = reinterpret_cast<B *>(values + (row0 + i) * ldv) + (int64_t)c * n;
-            uint32_t u = taken;
-            for (int s = 0; s < n; ++s) {
-                const int j = __builtin_ctz(u);
-                u &= u - 1;
+#pragma unroll
+            for (int s = 0; s < MT; ++s) {
+                if (s >= n) continue;
                 B x = 0;
 #pragma unroll
                 for (int jj = 0; jj < MT; ++jj)
-                    if (jj == j) x = (B)rr[i * NV + jj / VB][jj % VB];
+                    if (jj == js[s]) x = (B)rr[i * NV + jj / VB][jj % VB];
                 dst[s] = x;
             }
         }
