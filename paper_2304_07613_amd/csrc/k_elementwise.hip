@@ -80,15 +80,23 @@ __global__ __launch_bounds__(kBlock) void k_compress(
     }
     __syncthreads();
 
-    // copy the kept weights of the g rows, bit for bit, coalesced on output
+    // copy the kept weights of the g rows, bit for bit, coalesced on output;
+    // 8 rows' loads in flight before their stores
     const int nout = min(cpb, C - c_first) * n;
-    for (int i = 0; i < g; ++i) {
-        const B *src = reinterpret_cast<const B *>(W + (row0 + i) * ldw);
-        B *dst = reinterpret_cast<B *>(values + (row0 + i) * ldv) + (int64_t)c_first * n;
-        for (int p = t; p < nout; p += kBlock) {
-            const int cc = c_first + p / n;
-            dst[p] = src[(int64_t)cc * m + sel[p]];
+    const B *Wb = reinterpret_cast<const B *>(W);
+    B *Vb = reinterpret_cast<B *>(values);
+    for (int p = t; p < nout; p += kBlock) {
+        const int64_t col = (int64_t)(c_first + p / n) * m + sel[p];
+        const int64_t out = (int64_t)c_first * n + p;
+        int i = 0;
+        for (; i + 8 <= g; i += 8) {
+            B v[8];
+#pragma unroll
+            for (int b = 0; b < 8; ++b) v[b] = Wb[(row0 + i + b) * ldw + col];
+#pragma unroll
+            for (int b = 0; b < 8; ++b) Vb[(row0 + i + b) * ldv + out] = v[b];
         }
+        for (; i < g; ++i) Vb[(row0 + i) * ldv + out] = Wb[(row0 + i) * ldw + col];
     }
 }
 
