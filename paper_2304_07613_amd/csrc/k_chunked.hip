@@ -12,6 +12,12 @@
 //                 lower row) -- the same pairs, in the same order, as scanning
 //                 the sorted list of all pairs, since a pair that is not
 //                 eligible never becomes eligible again.
+//   k_p_compress_w the same greedy for chunks of at most 1024 (row, pattern)
+//                 pairs: one wave per chunk, each lane holding up to 16 pairs'
+//                 keys in registers with a mask of the pairs still eligible;
+//                 every step is a wave-wide maximum by shuffles, the pattern
+//                 counts live in registers (pattern p with lane p % 64), so a
+//                 workgroup of 4 waves converts 4 chunks with 28 KB of LDS.
 //   k_p_spmm      vector FMAs: the rows of a group are scattered over the
 //                 chunk, so rows share no operands; each wave owns 16 rows of
 //                 one chunk and 256 tokens, and finds each row's position in
@@ -128,6 +134,106 @@ __global__ __launch_bounds__(kBlock) void k_p_compress(const T *__restrict__ W, 
 
     // positions: patterns in order, rows of a group ascending; bit copies of W
     for (int r = t; r < S; r += kBlock) {
+        const int p = assigned[r];
+        int pos = p * g;
+        for (int q = 0; q < r; ++q) pos += assigned[q] == p;
+        index[(row0 + pos) * B + b] = (uint8_t)r;
+        for (int k = 0; k < n; ++k)
+            reinterpret_cast<Bt *>(values)[(row0 + pos) * ldv + (int64_t)b * n + k] =
+                reinterpret_cast<const Bt *>(W)[(row0 + r) * ldw + (int64_t)b * m + pat[p * n + k]];
+    }
+}
+
+// One wave per chunk, for chunks of at most kPwPairs * 64 pairs (see the
+// file comment); the same keys, eligibility and order as k_p_compress.
+constexpr int kPwWaves = 4;
+constexpr int kPwPairs = 16;       // pairs per lane
+constexpr int kPwWblk = 1024;      // S * m weights per chunk
+constexpr int kPwPat = 1024;       // P * n pattern offsets per chunk
+
+__device__ __forceinline__ void p_wave_sync() {
+    // this wave's LDS writes are done before its later LDS reads
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <typename T>
+__global__ __launch_bounds__(64 * kPwWaves) void k_p_compress_w(const T *__restrict__ W, int64_t ldw,
+                                                                T *__restrict__ values,
+                                                                uint8_t *__restrict__ index, int n,
+                                                                int m, int g, int P, int S, int B,
+                                                                int chunks) {
+    using Bt = typename Bits<T>::type;
+    __shared__ float wabs_all[kPwWaves][kPwWblk];
+    __shared__ uint8_t pat_all[kPwWaves][kPwPat];
+    __shared__ int assigned_all[kPwWaves][kPMaxS];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int id = blockIdx.x * kPwWaves + wave;
+    if (id >= chunks) return;  // whole waves; no workgroup barrier follows
+    float *wabs = wabs_all[wave];
+    uint8_t *pat = pat_all[wave];
+    int *assigned = assigned_all[wave];
+    const int c = id / B, b = id % B;
+    const int64_t row0 = (int64_t)c * S, ldv = (int64_t)B * n;
+
+    for (int i = lane; i < S * m; i += 64)
+        wabs[i] = p_abs(W + (row0 + i / m) * ldw + (int64_t)b * m + i % m);
+    for (int p = lane; p < P; p += 64) p_unrank(m, n, p, pat + p * n);
+    p_wave_sync();
+
+    // this lane's pairs j = lane + 64 q: key as in k_p_compress, row and pattern
+    unsigned long long key[kPwPairs];
+    uint32_t rp[kPwPairs];
+    uint32_t alive = 0;
+#pragma unroll
+    for (int q = 0; q < kPwPairs; ++q) {
+        const int j = lane + 64 * q;
+        key[q] = 0;
+        rp[q] = 0xffffu;
+        if (j < S * P) {
+            const int r = j / P, p = j - r * P;
+            float sc = 0.f;  // binary32, the pattern's offsets ascending, from +0
+            for (int k = 0; k < n; ++k) sc = sc + wabs[r * m + pat[p * n + k]];
+            const uint32_t bits = isnan(sc) ? 0x7fc00000u : __builtin_bit_cast(uint32_t, sc);
+            key[q] = ((unsigned long long)bits << 17) | (1ull << 16) | ((uint64_t)(255 - p) << 8) |
+                     (uint64_t)(255 - r);
+            rp[q] = ((uint32_t)r << 8) | (uint32_t)p;
+            alive |= 1u << q;
+        }
+    }
+    // pattern p's count lives in register p / 64 of lane p % 64 (P <= 256)
+    int cnt[4] = {0, 0, 0, 0};
+    for (int it = 0; it < S; ++it) {
+        unsigned long long k = 0;
+#pragma unroll
+        for (int q = 0; q < kPwPairs; ++q)
+            if ((alive >> q) & 1u) k = max(k, key[q]);
+        for (int off = 32; off > 0; off >>= 1) k = max(k, (unsigned long long)__shfl_xor(k, off));
+        // every step has a pair: the free rows equal the free pattern places
+        const int rw = 255 - (int)(k & 0xff), pw = 255 - (int)((k >> 8) & 0xff);
+        const int slot = pw >> 6;
+        int now = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (i == slot) now = __builtin_amdgcn_readlane(cnt[i], pw & 63) + 1;
+        if (lane == (pw & 63)) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (i == slot) cnt[i] = now;
+        }
+        if (lane == 0) assigned[rw] = pw;
+        const bool full = now >= g;
+#pragma unroll
+        for (int q = 0; q < kPwPairs; ++q) {
+            const uint32_t r = rp[q] >> 8, p = rp[q] & 0xffu;
+            if (r == (uint32_t)rw || (full && p == (uint32_t)pw)) alive &= ~(1u << q);
+        }
+    }
+    p_wave_sync();
+
+    // positions: patterns in order, rows of a group ascending; bit copies of W
+    for (int r = lane; r < S; r += 64) {
         const int p = assigned[r];
         int pos = p * g;
         for (int q = 0; q < r; ++q) pos += assigned[q] == p;
@@ -326,6 +432,20 @@ int p_pattern_count(int m, int n) { return p_binom(m, n); }
 nmg_status launch_p_compress(const nmg_p_layout *L, const void *W, int64_t ldw, void *values,
                              uint8_t *index, hipStream_t stream) {
     if (!p_fits(L)) return NMG_ERR_UNSUPPORTED;
+    const int64_t chunks = (int64_t)(L->M / L->S) * L->B;
+    if (L->S * L->P <= 64 * kPwPairs && L->S * L->m <= kPwWblk && L->P * L->n <= kPwPat &&
+        chunks <= INT32_MAX - kPwWaves) {
+        const unsigned blocks = (unsigned)((chunks + kPwWaves - 1) / kPwWaves);
+        if (L->dtype == NMG_F32)
+            hipLaunchKernelGGL((k_p_compress_w<float>), dim3(blocks), dim3(64 * kPwWaves), 0, stream,
+                               (const float *)W, ldw, (float *)values, index, L->n, L->m, L->g,
+                               L->P, L->S, L->B, (int)chunks);
+        else
+            hipLaunchKernelGGL((k_p_compress_w<_Float16>), dim3(blocks), dim3(64 * kPwWaves), 0,
+                               stream, (const _Float16 *)W, ldw, (_Float16 *)values, index, L->n,
+                               L->m, L->g, L->P, L->S, L->B, (int)chunks);
+        return launched();
+    }
     dim3 grid(L->M / L->S, L->B);
     if (L->dtype == NMG_F32)
         hipLaunchKernelGGL((k_p_compress<float>), grid, dim3(kBlock), 0, stream, (const float *)W,
