@@ -18,6 +18,9 @@
 //                 every step is a wave-wide maximum by shuffles, the pattern
 //                 counts live in registers (pattern p with lane p % 64), so a
 //                 workgroup of 4 waves converts 4 chunks with 28 KB of LDS.
+//   k_p_refine_w  the same swap search for chunks of at most 1024 pairs: one
+//                 wave per chunk, each lane owning up to 4 rows, the round's
+//                 flag a wave vote.
 //   k_p_spmm      vector FMAs: the rows of a group are scattered over the
 //                 chunk, so rows share no operands; each wave owns 16 rows of
 //                 one chunk and 256 tokens, and finds each row's position in
@@ -244,6 +247,90 @@ __global__ __launch_bounds__(64 * kPwWaves) void k_p_compress_w(const T *__restr
     }
 }
 
+// The swap search with one wave per chunk (at most kPwPairs * 64 pairs): the
+// same rounds, gains and tie rules as k_p_refine.
+template <typename T>
+__global__ __launch_bounds__(64 * kPwWaves) void k_p_refine_w(const T *__restrict__ W, int64_t ldw,
+                                                              T *__restrict__ values,
+                                                              uint8_t *__restrict__ index, int n,
+                                                              int m, int g, int P, int S, int B,
+                                                              int chunks) {
+    using Bt = typename Bits<T>::type;
+    __shared__ float wabs_all[kPwWaves][kPwWblk];
+    __shared__ float score_all[kPwWaves][64 * kPwPairs];
+    __shared__ uint8_t pat_all[kPwWaves][kPwPat];
+    __shared__ int pa_all[kPwWaves][kPMaxS];
+    __shared__ int best_all[kPwWaves][kPMaxS];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int id = blockIdx.x * kPwWaves + wave;
+    if (id >= chunks) return;  // whole waves; no workgroup barrier follows
+    float *wabs = wabs_all[wave], *score = score_all[wave];
+    uint8_t *pat = pat_all[wave];
+    int *pa = pa_all[wave], *best = best_all[wave];
+    const int c = id / B, b = id % B;
+    const int64_t row0 = (int64_t)c * S, ldv = (int64_t)B * n;
+
+    for (int i = lane; i < S * m; i += 64)
+        wabs[i] = p_abs(W + (row0 + i / m) * ldw + (int64_t)b * m + i % m);
+    for (int p = lane; p < P; p += 64) p_unrank(m, n, p, pat + p * n);
+    // the packing to start from (a malformed index leaves rows on pattern 0
+    // and never reads outside the tables)
+    for (int r = lane; r < S; r += 64) pa[r] = 0;
+    p_wave_sync();
+    for (int j = lane; j < S; j += 64) pa[min((int)index[(row0 + j) * B + b], S - 1)] = j / g;
+    p_wave_sync();
+    for (int i = lane; i < S * P; i += 64) {
+        const int r = i / P, p = i % P;
+        float sc = 0.f;  // binary32, the pattern's offsets ascending, from +0
+        for (int k = 0; k < n; ++k) sc = sc + wabs[r * m + pat[p * n + k]];
+        score[i] = sc;
+    }
+    p_wave_sync();
+    for (int round = 0; round < 8 * S; ++round) {
+        bool found = false;
+        for (int r = lane; r < S; r += 64) {
+            const int a = pa[r];
+            int bq = -1;
+            double bg = 0.0;
+            for (int q = 0; q < S; ++q) {
+                const int e = pa[q];
+                if (e == a) continue;
+                const double gain = ((double)score[r * P + e] + (double)score[q * P + a]) -
+                                    ((double)score[r * P + a] + (double)score[q * P + e]);
+                if (gain > bg) {  // strictly larger: ties keep the lower q
+                    bg = gain;
+                    bq = q;
+                }
+            }
+            best[r] = bq;
+            found = found || bq >= 0;
+        }
+        if (!__any(found)) break;  // uniform across the wave
+        p_wave_sync();
+        for (int r = lane; r < S; r += 64) {
+            const int q = best[r];
+            if (q > r && best[q] == r) {  // mutual best partners: disjoint pairs
+                const int a = pa[r];
+                pa[r] = pa[q];
+                pa[q] = a;
+            }
+        }
+        p_wave_sync();
+    }
+    p_wave_sync();
+
+    // stored like nmg_p_compress's result: patterns in order, rows of a group ascending
+    for (int r = lane; r < S; r += 64) {
+        const int p = pa[r];
+        int pos = p * g;
+        for (int q = 0; q < r; ++q) pos += pa[q] == p;
+        index[(row0 + pos) * B + b] = (uint8_t)r;
+        for (int k = 0; k < n; ++k)
+            reinterpret_cast<Bt *>(values)[(row0 + pos) * ldv + (int64_t)b * n + k] =
+                reinterpret_cast<const Bt *>(W)[(row0 + r) * ldw + (int64_t)b * m + pat[p * n + k]];
+    }
+}
+
 template <typename T>
 __global__ __launch_bounds__(kBlock) void k_p_densify(const T *__restrict__ values,
                                                       const uint8_t *__restrict__ index,
@@ -460,6 +547,20 @@ nmg_status launch_p_compress(const nmg_p_layout *L, const void *W, int64_t ldw, 
 nmg_status launch_p_refine(const nmg_p_layout *L, const void *W, int64_t ldw, void *values,
                            uint8_t *index, hipStream_t stream) {
     if (!p_fits(L)) return NMG_ERR_UNSUPPORTED;
+    const int64_t chunks = (int64_t)(L->M / L->S) * L->B;
+    if (L->S * L->P <= 64 * kPwPairs && L->S * L->m <= kPwWblk && L->P * L->n <= kPwPat &&
+        chunks <= INT32_MAX - kPwWaves) {
+        const unsigned blocks = (unsigned)((chunks + kPwWaves - 1) / kPwWaves);
+        if (L->dtype == NMG_F32)
+            hipLaunchKernelGGL((k_p_refine_w<float>), dim3(blocks), dim3(64 * kPwWaves), 0, stream,
+                               (const float *)W, ldw, (float *)values, index, L->n, L->m, L->g,
+                               L->P, L->S, L->B, (int)chunks);
+        else
+            hipLaunchKernelGGL((k_p_refine_w<_Float16>), dim3(blocks), dim3(64 * kPwWaves), 0,
+                               stream, (const _Float16 *)W, ldw, (_Float16 *)values, index, L->n,
+                               L->m, L->g, L->P, L->S, L->B, (int)chunks);
+        return launched();
+    }
     dim3 grid(L->M / L->S, L->B);
     if (L->dtype == NMG_F32)
         hipLaunchKernelGGL((k_p_refine<float>), grid, dim3(kBlock), 0, stream, (const float *)W,
