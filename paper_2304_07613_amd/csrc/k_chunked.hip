@@ -25,6 +25,10 @@
 //                 chunk, so rows share no operands; each wave owns 16 rows of
 //                 one chunk and 256 tokens, and finds each row's position in
 //                 every block column through an inverse table built in LDS.
+//                 When m <= 32 and the chunk has at least 64 rows, the X rows
+//                 of a window of block columns are staged in LDS (binary32, 32
+//                 rows) and every row reads the rows its pattern selects from
+//                 there, instead of gathering them from global memory.
 //   k_p_densify   one thread per stored block.
 //   k_p_refine    the swap search of the paper's GPU converter (Section 5.2),
 //                 in a fixed order: one workgroup per chunk, one thread per
@@ -44,6 +48,7 @@ constexpr int kPMaxPat = 4096;     // P * n pattern offsets held in LDS
 constexpr int kPRowsWave = 16;
 constexpr int kPTokens = 256;      // 4 per lane
 constexpr int kPWin = 32;          // block columns per inverse table
+constexpr int kPStageRows = 32;    // X rows staged per window by k_p_spmm (256 tokens each)
 
 __host__ __device__ inline int p_binom(int m, int n) {
     int64_t v = 1;
@@ -430,7 +435,7 @@ __global__ __launch_bounds__(kBlock) void k_p_refine(const T *__restrict__ W, in
 
 constexpr int kPMaxWaves = kPMaxS / kPRowsWave;  // 16 waves cover the largest chunk
 
-template <typename T>
+template <typename T, bool STAGED>
 __global__ __launch_bounds__(64 * kPMaxWaves) void k_p_spmm(const T *__restrict__ values,
                                                    const uint8_t *__restrict__ index,
                                                    const T *__restrict__ X, int64_t ldx,
@@ -439,6 +444,7 @@ __global__ __launch_bounds__(64 * kPMaxWaves) void k_p_spmm(const T *__restrict_
                                                    bool xvec) {
     __shared__ uint8_t pat[kPMaxPat];
     __shared__ uint8_t inv[kPWin * kPMaxS];  // position of chunk row rr in block column w
+    __shared__ v4f xs[STAGED ? kPStageRows * 64 : 1];  // staged X rows, 4 tokens per lane
     const int c = blockIdx.x / tok_tiles, tt = blockIdx.x % tok_tiles;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -455,13 +461,23 @@ __global__ __launch_bounds__(64 * kPMaxWaves) void k_p_spmm(const T *__restrict_
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[r][j] = 0.f;
 
-    for (int b0 = 0; b0 < B; b0 += kPWin) {
-        const int nb = min(kPWin, B - b0);
-        __syncthreads();  // the previous window's table is no longer read
+    // block columns per window (host checked for STAGED: m <= kPStageRows)
+    const int nbw = STAGED ? min(kPWin, kPStageRows / m) : kPWin;
+    for (int b0 = 0; b0 < B; b0 += nbw) {
+        const int nb = min(nbw, B - b0);
+        __syncthreads();  // the previous window's table and rows are no longer read
         for (int i = threadIdx.x; i < nb * S; i += blockDim.x) {
             const int w = i / S, jpos = i % S;
             const int rr = min((int)index[(row0 + jpos) * B + b0 + w], S - 1);
             inv[w * kPMaxS + rr] = (uint8_t)jpos;
+        }
+        if constexpr (STAGED) {
+            // X rows b0 m .. (b0 + nb) m - 1 (all inside K = B m), this tile's tokens
+            for (int i = threadIdx.x; i < nb * m * 64; i += blockDim.x) {
+                const int xr = i >> 6, l = i & 63;
+                const int t4 = tt * kPTokens + 4 * l;
+                xs[i] = load4<T>(X + ((int64_t)b0 * m + xr) * ldx + t4, N - t4, xvec);
+            }
         }
         __syncthreads();
         for (int w = 0; w < nb; ++w) {
@@ -476,7 +492,8 @@ __global__ __launch_bounds__(64 * kPMaxWaves) void k_p_spmm(const T *__restrict_
                 const T *v = values + (row0 + jpos) * ldv + (int64_t)b * n;
                 for (int k = 0; k < n; ++k) {
                     const float wv = (float)v[k];
-                    const v4f x = load4<T>(X + ((int64_t)b * m + off[k]) * ldx + tok, valid, xvec);
+                    const v4f x = STAGED ? xs[(w * m + off[k]) * 64 + lane]
+                                         : load4<T>(X + ((int64_t)b * m + off[k]) * ldx + tok, valid, xvec);
 #pragma unroll
                     for (int j = 0; j < 4; ++j) acc[r][j] = fmaf(wv, x[j], acc[r][j]);
                 }
@@ -599,15 +616,21 @@ nmg_status launch_p_spmm(const nmg_p_layout *L, const void *values, const uint8_
     // binary32 X rows on 16-byte boundaries are read 4 tokens at a time
     const size_t es = elem_size(L->dtype);
     const bool xvec = aligned(X, 4 * es) && ldx % 4 == 0;
-    if (L->dtype == NMG_F32)
-        hipLaunchKernelGGL((k_p_spmm<float>), dim3((unsigned)grid), dim3(64 * waves), 0, stream,
-                           (const float *)values, index, (const float *)X, ldx, (float *)Y, ldy, N,
-                           L->n, L->m, L->g, L->P, L->S, L->B, tok_tiles, xvec);
-    else
-        hipLaunchKernelGGL((k_p_spmm<_Float16>), dim3((unsigned)grid), dim3(64 * waves), 0,
-                           stream, (const _Float16 *)values, index, (const _Float16 *)X, ldx,
-                           (_Float16 *)Y, ldy, N, L->n, L->m, L->g, L->P, L->S, L->B, tok_tiles,
-                           xvec);
+    // staging pays when the chunk has enough rows (4 waves or more) to share
+    // each staged row; small chunks gather (measured on the 3072 x 768 sweep)
+    const bool staged = L->m <= kPStageRows && L->S >= 64;
+#define NMG_P_SPMM(T, ST)                                                                         \
+    hipLaunchKernelGGL((k_p_spmm<T, ST>), dim3((unsigned)grid), dim3(64 * waves), 0, stream,       \
+                       (const T *)values, index, (const T *)X, ldx, (T *)Y, ldy, N, L->n, L->m,    \
+                       L->g, L->P, L->S, L->B, tok_tiles, xvec)
+    if (L->dtype == NMG_F32) {
+        if (staged) NMG_P_SPMM(float, true);
+        else NMG_P_SPMM(float, false);
+    } else {
+        if (staged) NMG_P_SPMM(_Float16, true);
+        else NMG_P_SPMM(_Float16, false);
+    }
+#undef NMG_P_SPMM
     return launched();
 }
 
