@@ -103,23 +103,35 @@ __global__ __launch_bounds__(kBlock) void k_compress(
 // --------------------------------------------------- compress, thread per chunk
 
 // For m <= MT (MT = 4, 8, 16 or 32): one thread owns one (group, chunk).  It
-// reads the chunk's m columns down the g rows (one vector load per row when
-// the chunk starts on a 16-byte boundary, 4 rows in flight at a time), sums
+// reads the chunk's m columns down the g rows (16-byte vector loads when rows
+// and chunks are whole vectors, 4 rows in flight at a time), sums
 // the scores in binary32 in row order, selects the n largest in registers
 // (the same order as k_compress: key bits, ties to the lower offset; n passes
 // of the first maximum for n <= 4, counted ranks otherwise), and writes the
 // indices and the kept weights of the g rows.  Adjacent threads own adjacent
-// chunks, so every load and store is coalesced across the wave, and W is read
-// exactly once.
+// chunks (a row's last chunk is followed by the next group's first), so the
+// loads and stores are coalesced across the wave, and W is read exactly once.
 template <typename T, int MT>
 __global__ __launch_bounds__(kBlock) void k_compress_chunk(
     const T *__restrict__ W, int64_t ldw, T *__restrict__ values,
-    uint8_t *__restrict__ indices, int K, int n, int m, int g, int C, bool vec) {
+    uint8_t *__restrict__ indices, int K, int n, int m, int g, int C, bool vec,
+    uint32_t pairs) {
     using B = typename Bits<T>::type;
     constexpr int VB = 16 / sizeof(T);            // elements per 16-byte vector
-    const int G = blockIdx.x;
-    const int c = blockIdx.y * kBlock + threadIdx.x;
-    if (c >= C) return;
+    // pairs > 0: the (group, chunk) pairs are numbered group-major across the
+    // whole grid, so every thread owns a chunk however few chunks a row has;
+    // pairs == 0 (more pairs than 31 bits hold): a row of groups per grid row
+    int G, c;
+    if (pairs) {
+        const uint32_t p = blockIdx.x * kBlock + threadIdx.x;
+        if (p >= pairs) return;
+        G = (int)(p / (uint32_t)C);
+        c = (int)(p - (uint32_t)G * (uint32_t)C);
+    } else {
+        G = blockIdx.x;
+        c = blockIdx.y * kBlock + threadIdx.x;
+        if (c >= C) return;
+    }
     const int w = min(m, K - c * m);              // chunk width
     const int64_t ldv = (int64_t)C * n;
     const int64_t row0 = (int64_t)G * g;
@@ -130,21 +142,28 @@ __global__ __launch_bounds__(kBlock) void k_compress_chunk(
     for (int j = 0; j < MT; ++j) score[j] = 0.0f;
     typedef B BV __attribute__((ext_vector_type(VB)));
     constexpr int NV = MT / VB + (MT % VB != 0);
-    // Small groups (g rows of whole 16-byte vectors, 16 vectors at most): every
-    // row's chunk is loaded at once and kept in registers, and the kept
-    // weights are picked from there -- one round trip to memory.
+    // Small groups (g <= RROWS rows of whole 16-byte vectors): every row's
+    // chunk is loaded at once and kept in registers, and the kept weights are
+    // picked from there -- one round trip to memory.  The pick is an unrolled
+    // select over MT offsets per kept slot and row, so RROWS keeps it near
+    // 1024 selects (none for MT = 32): larger kernels outgrow the instruction
+    // cache and ran 3x slower.
+    // With vec, every chunk (the last one too) is whole 16-byte vectors: a
+    // vector past a short last chunk's end is loaded from its last vector
+    // instead (in bounds), and the scores of columns j >= w are never keys.
     constexpr int RMAX = 16;
-    const bool whole = vec && w == m;
-    const bool in_regs = whole && g * NV <= RMAX;
-    BV rr[RMAX];
+    constexpr int RROWS = MT > 16 ? 0 : (RMAX / NV < 1024 / (MT * MT) ? RMAX / NV : 1024 / (MT * MT));
+    const bool in_regs = RROWS > 0 && vec && g <= RROWS;
+    BV rr[RROWS * NV + (RROWS == 0)];
     if (in_regs) {
 #pragma unroll
-        for (int q = 0; q < RMAX; ++q) {
+        for (int q = 0; q < RROWS * NV; ++q) {
             const int i = q / NV, v = q % NV;
-            if (i < g && v * VB < m) rr[q] = *reinterpret_cast<const BV *>(W + (row0 + i) * ldw + col0 + v * VB);
+            if (i < g && v * VB < m)
+                rr[q] = *reinterpret_cast<const BV *>(W + (row0 + i) * ldw + col0 + min(v * VB, w - VB));
         }
 #pragma unroll
-        for (int q = 0; q < RMAX; ++q) {   // rows in ascending order
+        for (int q = 0; q < RROWS * NV; ++q) {   // rows in ascending order
             const int i = q / NV, v = q % NV;
             if (i < g && v * VB < m)
 #pragma unroll
@@ -156,14 +175,14 @@ __global__ __launch_bounds__(kBlock) void k_compress_chunk(
         // every row has landed (the scores needed them): said explicitly, so
         // that the stores below are not each preceded by a wait for memory
         wait_all_memory();
-    } else if (whole) {
-        // m % VB == 0 here: whole 16-byte vectors.  Rows come 4 at a time
-        // (the loads of 4 rows in flight together), added in row order.
+    } else if (vec) {
+        // Rows come in batches (the loads of a batch in flight together),
+        // added in row order.
         auto load_row = [&](int i, BV (&r)[NV]) {
             const T *p = W + (row0 + i) * ldw + col0;
 #pragma unroll
             for (int v = 0; v < NV; ++v)
-                if (v * VB < m) r[v] = *reinterpret_cast<const BV *>(p + v * VB);
+                if (v * VB < m) r[v] = *reinterpret_cast<const BV *>(p + min(v * VB, w - VB));
         };
         auto add_row = [&](const BV (&r)[NV]) {
 #pragma unroll
@@ -175,8 +194,9 @@ __global__ __launch_bounds__(kBlock) void k_compress_chunk(
                         if (j < MT) score[j] = score[j] + fabsf((float)__builtin_bit_cast(T, (B)r[v][e]));
                     }
         };
-        // 4 rows per batch: their loads in flight together
-        constexpr int RB = 4;
+        // up to 4 rows per batch (16 vectors at most): their loads in flight
+        // together
+        constexpr int RB = RMAX / NV < 4 ? RMAX / NV : 4;
         int i = 0;
         for (; i + RB <= g; i += RB) {
             BV r[RB][NV];
@@ -191,11 +211,15 @@ __global__ __launch_bounds__(kBlock) void k_compress_chunk(
             add_row(r0);
         }
     } else {
+        // element loads, all MT of a row in flight: a column past the chunk's
+        // end is loaded from its last column (in bounds) and never becomes a key
         for (int i = 0; i < g; ++i) {
             const T *p = W + (row0 + i) * ldw + col0;
+            T e[MT];
 #pragma unroll
-            for (int j = 0; j < MT; ++j)
-                if (j < w) score[j] = score[j] + fabsf((float)p[j]);
+            for (int j = 0; j < MT; ++j) e[j] = p[min(j, w - 1)];
+#pragma unroll
+            for (int j = 0; j < MT; ++j) score[j] = score[j] + fabsf((float)e[j]);
         }
     }
     // order keys: non-negative floats order like their bits; NaN above +inf
@@ -254,7 +278,7 @@ __global__ __launch_bounds__(kBlock) void k_compress_chunk(
             u &= u - 1;
         }
 #pragma unroll
-        for (int i = 0; i < RMAX / NV; ++i) {
+        for (int i = 0; i < RROWS; ++i) {
             if (i >= g) continue;
             B *dst = reinterpret_cast<B *>(values + (row0 + i) * ldv) + (int64_t)c * n;
 #pragma unroll
@@ -324,12 +348,17 @@ namespace nmg_internal {
 template <typename T>
 nmg_status launch_compress_chunk(const nmg_layout *L, const void *W, int64_t ldw, void *values,
                                  uint8_t *indices, hipStream_t stream) {
+    // whole 16-byte vectors: the rows, every chunk and the last chunk
     const bool vec = aligned(W, 16) && (ldw * sizeof(T)) % 16 == 0 &&
-                     (L->m * sizeof(T)) % 16 == 0;
-    dim3 grid(L->M / L->g, (L->C + kBlock - 1) / kBlock);
+                     (L->m * sizeof(T)) % 16 == 0 && (L->K * sizeof(T)) % 16 == 0;
+    const int64_t pairs = (int64_t)(L->M / L->g) * L->C;
+    const bool flat = pairs <= INT32_MAX - kBlock;
+    const dim3 grid = flat ? dim3((unsigned)((pairs + kBlock - 1) / kBlock))
+                           : dim3(L->M / L->g, (L->C + kBlock - 1) / kBlock);
 #define NMG_CHUNK(MT)                                                                          \
     hipLaunchKernelGGL((k_compress_chunk<T, MT>), grid, dim3(kBlock), 0, stream, (const T *)W,   \
-                       ldw, (T *)values, indices, L->K, L->n, L->m, L->g, L->C, vec)
+                       ldw, (T *)values, indices, L->K, L->n, L->m, L->g, L->C, vec,           \
+                       flat ? (uint32_t)pairs : 0u)
     if (L->m <= 4) NMG_CHUNK(4);
     else if (L->m <= 8) NMG_CHUNK(8);
     else if (L->m <= 16) NMG_CHUNK(16);
