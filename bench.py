@@ -406,6 +406,8 @@ def chunked(ctx, args):
                "us_swap_search": round(timed(lambda: nmg.p_refine(W, pidx, PL)), 2),
                "us_spmm_group": round(timed(lambda: nmg.spmm(v, idx, X, L)), 2),
                "us_spmm_chunked": round(timed(lambda: nmg.p_spmm(pv, pidx, X, PL)), 2),
+               "us_spmm_chunked_valu": round(timed(lambda: nmg.p_spmm(pv, pidx, X, PL, "valu")), 2),
+               "us_spmm_chunked_mfma": round(timed(lambda: nmg.p_spmm(pv, pidx, X, PL, "mfma")), 2),
                "group_kernel": nmg.auto_kernel(L, lin.N)}
         rec["tflops_spmm_chunked"] = round(lin.useful_flop / rec["us_spmm_chunked"] / 1e6, 2)
         rec["tflops_spmm_group"] = round(lin.useful_flop / rec["us_spmm_group"] / 1e6, 2)

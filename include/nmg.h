@@ -266,13 +266,26 @@ nmg_status nmg_p_compress(const nmg_p_layout *layout, const void *W, int64_t ldw
 nmg_status nmg_p_refine(const nmg_p_layout *layout, const void *W, int64_t ldw, void *values,
                         uint8_t *index, hipStream_t stream);
 
-/* Y = W_s * X for the chunked layout: X K x N (ldx >= N), Y M x N (ldy >= N),
- * element-aligned; binary32 accumulation in ascending column order of each
- * row.  An index that is not a permutation in every chunk column gives
- * unspecified Y, but no read leaves the buffers. */
+/* Y = W_s * X for the chunked layout (the product of Section 5 on this
+ * layout): X K x N (ldx >= N), Y M x N (ldy >= N), element-aligned; binary32
+ * accumulation (binary16 inputs widened exactly).  An index that is not a
+ * permutation in every chunk column gives unspecified Y, but no read leaves
+ * the buffers.  Uses NMG_KERNEL_AUTO. */
 nmg_status nmg_p_spmm(const nmg_p_layout *layout, const void *values, const uint8_t *index,
                       const void *X, int64_t ldx, int64_t N, void *Y, int64_t ldy,
                       hipStream_t stream);
+
+/* nmg_p_spmm with an explicit kernel:
+ *   NMG_KERNEL_VALU  vector FMAs, each row's kept products in ascending column
+ *                    order; every valid layout.
+ *   NMG_KERNEL_MFMA  binary32 matrix cores on the blocks expanded to m values
+ *                    (n / m of the products useful); m <= 32, else
+ *                    NMG_ERR_UNSUPPORTED.
+ *   NMG_KERNEL_AUTO  MFMA when 4 n >= m and m <= 32, else VALU.
+ * Any other kernel: NMG_ERR_UNSUPPORTED.  Arguments as nmg_p_spmm. */
+nmg_status nmg_p_spmm_with(const nmg_p_layout *layout, nmg_kernel kernel, const void *values,
+                           const uint8_t *index, const void *X, int64_t ldx, int64_t N, void *Y,
+                           int64_t ldy, hipStream_t stream);
 
 /* Chunked layout -> dense W_out (M x K, leading dimension ldw >= K). */
 nmg_status nmg_p_densify(const nmg_p_layout *layout, const void *values, const uint8_t *index,

@@ -261,16 +261,24 @@ nmg_status nmg_p_refine(const nmg_p_layout *L, const void *W, int64_t ldw, void 
     return launch_p_refine(L, W, ldw, values, index, stream);
 }
 
-nmg_status nmg_p_spmm(const nmg_p_layout *L, const void *values, const uint8_t *index,
-                      const void *X, int64_t ldx, int64_t N, void *Y, int64_t ldy,
-                      hipStream_t stream) {
+nmg_status nmg_p_spmm_with(const nmg_p_layout *L, nmg_kernel kernel, const void *values,
+                           const uint8_t *index, const void *X, int64_t ldx, int64_t N, void *Y,
+                           int64_t ldy, hipStream_t stream) {
     nmg_status st = check_p_layout(L);
     if (st != NMG_OK) return st;
+    if (kernel != NMG_KERNEL_AUTO && kernel != NMG_KERNEL_VALU && kernel != NMG_KERNEL_MFMA)
+        return NMG_ERR_UNSUPPORTED;
     if (!values || !index || !X || !Y) return NMG_ERR_NULL;
     if (N < 1 || N > INT32_MAX || ldx < N || ldy < N) return NMG_ERR_PARAM;
     const size_t es = elem_size(L->dtype);
     if (!aligned(X, es) || !aligned(values, es) || !aligned(Y, es)) return NMG_ERR_ALIGN;
-    return launch_p_spmm(L, values, index, X, ldx, (int)N, Y, ldy, stream);
+    return launch_p_spmm(L, kernel, values, index, X, ldx, (int)N, Y, ldy, stream);
+}
+
+nmg_status nmg_p_spmm(const nmg_p_layout *L, const void *values, const uint8_t *index,
+                      const void *X, int64_t ldx, int64_t N, void *Y, int64_t ldy,
+                      hipStream_t stream) {
+    return nmg_p_spmm_with(L, NMG_KERNEL_AUTO, values, index, X, ldx, N, Y, ldy, stream);
 }
 
 nmg_status nmg_p_densify(const nmg_p_layout *L, const void *values, const uint8_t *index,

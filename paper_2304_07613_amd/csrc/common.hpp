@@ -117,9 +117,9 @@ nmg_status launch_p_densify(const nmg_p_layout *L, const void *values, const uin
                             void *W_out, int64_t ldw, hipStream_t stream);
 nmg_status launch_p_refine(const nmg_p_layout *L, const void *W, int64_t ldw, void *values,
                            uint8_t *index, hipStream_t stream);
-nmg_status launch_p_spmm(const nmg_p_layout *L, const void *values, const uint8_t *index,
-                         const void *X, int64_t ldx, int N, void *Y, int64_t ldy,
-                         hipStream_t stream);
+nmg_status launch_p_spmm(const nmg_p_layout *L, nmg_kernel kernel, const void *values,
+                         const uint8_t *index, const void *X, int64_t ldx, int N, void *Y,
+                         int64_t ldy, hipStream_t stream);
 nmg_status spmm_half(const SpmmArgs &a);
 
 }  // namespace nmg_internal

@@ -29,6 +29,16 @@
 //                 of a window of block columns are staged in LDS (binary32, 32
 //                 rows) and every row reads the rows its pattern selects from
 //                 there, instead of gathering them from global memory.
+//   k_p_spmm_mfma matrix cores on the expanded blocks: in one block column a
+//                 row's block is an m-vector with m - n zeros, and all S rows
+//                 of the chunk read the same m rows of X there, so the chunk
+//                 times X is a dense contraction over K of which n / m of the
+//                 products are useful.  Each workgroup owns 64 rows x 256
+//                 tokens; per window of up to 32 k-columns every stored block
+//                 writes its expanded m values into a k-major LDS tile at its
+//                 chunk row (no inverse table), the X rows are staged in
+//                 binary32, and each wave runs 4 x 4 v_mfma_f32_16x16x4f32
+//                 tiles (64 rows x 64 tokens) over them.
 //   k_p_densify   one thread per stored block.
 //   k_p_refine    the swap search of the paper's GPU converter (Section 5.2),
 //                 in a fixed order: one workgroup per chunk, one thread per
@@ -516,6 +526,132 @@ bool p_fits(const nmg_p_layout *L) {
            L->S <= kPMaxS;
 }
 
+// ------------------------------------------------ product on matrix cores
+
+constexpr int kPmRows = 64;               // rows per workgroup
+constexpr int kPmTok = 256;               // tokens per workgroup (64 per wave)
+constexpr int kPmKw = 32;                 // k columns per window, at most
+constexpr int kPmLda = kPmRows + 16;      // padded leading dimensions: the 4 k
+constexpr int kPmLdb = kPmTok + 16;       // rows of an operand read fall on 4
+                                          // disjoint sets of 16 banks
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_p_spmm_mfma(const T *__restrict__ values,
+                                                     const uint8_t *__restrict__ index,
+                                                     const T *__restrict__ X, int64_t ldx,
+                                                     T *__restrict__ Y, int64_t ldy, int M, int N,
+                                                     int n, int m, int g, int P, int S, int B,
+                                                     int row_tiles, int tok_tiles, bool xvec) {
+    __shared__ uint8_t pat[kPMaxPat];
+    __shared__ float As[kPmKw * kPmLda];   // expanded weights, As[k][row]
+    __shared__ float Bs[kPmKw * kPmLdb];   // X rows, Bs[k][token]
+    const int tile = xcd_tile(blockIdx.x, row_tiles * tok_tiles);
+    const int tt = tile / row_tiles, rt = tile - tt * row_tiles;
+    const int R0 = rt * kPmRows, t0 = tt * kPmTok;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lr = lane & 15, lk = lane >> 4;
+    const int64_t ldv = (int64_t)B * n;
+    // the stored rows whose blocks can land in this tile: its chunks'
+    const int s_lo = (R0 / S) * S;
+    const int s_hi = min(M, (min(M, R0 + kPmRows) + S - 1) / S * S);
+    const int ns = s_hi - s_lo;
+    // whole 256-token tile of 16-byte aligned rows: vector loads, no tail
+    const bool xfull = xvec && t0 + kPmTok <= N;
+
+    for (int p = tid; p < P; p += 256) p_unrank(m, n, p, pat + p * n);
+
+    v4f acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+
+    const int nbw = kPmKw / m;   // block columns per window (m <= kPmKw, host checked)
+    for (int b0 = 0; b0 < B; b0 += nbw) {
+        const int nb = min(nbw, B - b0);
+        const int kw = nb * m, kw4 = (kw + 3) & ~3;
+        // X rows b0 m .. b0 m + kw - 1 of this token tile into registers first
+        // (rows past kw re-read row kw - 1 and are stored as zeros), so the
+        // loads are in flight together
+        v4f xr[kPmKw / 4];
+        const int kx = tid >> 6, tx = t0 + 4 * lane;
+#pragma unroll
+        for (int q = 0; q < kPmKw / 4; ++q) {
+            const int k = min(kx + 4 * q, kw - 1);
+            const T *src = X + ((int64_t)b0 * m + k) * ldx + tx;
+            if (xfull) {
+                if constexpr (std::is_same<T, float>::value) {
+                    xr[q] = *reinterpret_cast<const v4f *>(src);
+                } else {
+                    const h4 h = *reinterpret_cast<const h4 *>(src);
+                    xr[q] = v4f{(float)h[0], (float)h[1], (float)h[2], (float)h[3]};
+                }
+            } else {
+                xr[q] = load4<T>(src, N - tx, xvec);
+            }
+        }
+        __syncthreads();  // the previous window is no longer read
+        // A: every stored block of the tile's chunks writes its expanded m
+        // values at its chunk row; k columns kw .. kw4 - 1 are zero
+        for (int i = tid; i < (kw4 - kw) * kPmRows; i += 256)
+            As[(kw + i / kPmRows) * kPmLda + i % kPmRows] = 0.f;
+        for (int i = tid; i < ns * nb; i += 256) {
+            const int j = i / nb, w = i - j * nb;
+            const int Rs = s_lo + j;                         // stored row
+            const int js = Rs % S;                           // its slot in the chunk
+            const int rho = min((int)index[(int64_t)Rs * B + b0 + w], S - 1);  // clamped
+            const int r = Rs - js + rho - R0;                // its row in the tile
+            if (r < 0 || r >= kPmRows) continue;
+            const uint8_t *off = pat + (js / g) * n;
+            const T *v = values + (int64_t)Rs * ldv + (int64_t)(b0 + w) * n;
+            float *a = As + (w * m) * kPmLda + r;
+            int s = 0;
+            for (int k = 0; k < m; ++k) {
+                float x = 0.f;
+                if (s < n && off[s] == k) x = (float)v[s++];
+                a[k * kPmLda] = x;
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < kPmKw / 4; ++q) {
+            const int k = kx + 4 * q;
+            if (k < kw4)
+                *reinterpret_cast<v4f *>(Bs + k * kPmLdb + 4 * lane) =
+                    k < kw ? xr[q] : v4f{0.f, 0.f, 0.f, 0.f};
+        }
+        __syncthreads();
+        // 16 x 16 x 4 steps: lane (lr, lk) brings A[row lr][k lk] and
+        // B[k lk][token lr]; row tiles i and token tiles j of this wave
+        for (int k0 = 0; k0 < kw4; k0 += 4) {
+            float a[4], bx[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) a[i] = As[(k0 + lk) * kPmLda + 16 * i + lr];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) bx[j] = Bs[(k0 + lk) * kPmLdb + 64 * wave + 16 * j + lr];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], bx[j], acc[i][j], 0, 0, 0);
+        }
+    }
+    // acc[i][j][e] = Y[R0 + 16 i + 4 lk + e][t0 + 64 wave + 16 j + lr]
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int row = R0 + 16 * i + 4 * lk + e;
+            if (row >= M) continue;
+            T *y = Y + (int64_t)row * ldy;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int t = t0 + 64 * wave + 16 * j + lr;
+                if (t < N) y[t] = (T)acc[i][j][e];
+            }
+        }
+}
+
 }  // namespace
 
 namespace nmg_internal {
@@ -605,17 +741,35 @@ nmg_status launch_p_densify(const nmg_p_layout *L, const void *values, const uin
     return launched();
 }
 
-nmg_status launch_p_spmm(const nmg_p_layout *L, const void *values, const uint8_t *index,
-                         const void *X, int64_t ldx, int N, void *Y, int64_t ldy,
-                         hipStream_t stream) {
+nmg_status launch_p_spmm(const nmg_p_layout *L, nmg_kernel kernel, const void *values,
+                         const uint8_t *index, const void *X, int64_t ldx, int N, void *Y,
+                         int64_t ldy, hipStream_t stream) {
     if (!p_fits(L)) return NMG_ERR_UNSUPPORTED;
+    const size_t es = elem_size(L->dtype);
+    const bool xvec = aligned(X, 4 * es) && ldx % 4 == 0;
+    // matrix cores when a quarter or more of the expanded products are useful
+    if (kernel == NMG_KERNEL_AUTO) kernel = 4 * L->n >= L->m && L->m <= kPmKw ? NMG_KERNEL_MFMA
+                                                                          : NMG_KERNEL_VALU;
+    if (kernel == NMG_KERNEL_MFMA) {
+        if (L->m > kPmKw) return NMG_ERR_UNSUPPORTED;
+        const int row_tiles = (L->M + kPmRows - 1) / kPmRows;
+        const int tok_tiles = (N + kPmTok - 1) / kPmTok;
+        const int64_t grid = (int64_t)row_tiles * tok_tiles;
+        if (grid > INT32_MAX) return NMG_ERR_PARAM;
+#define NMG_P_MFMA(T)                                                                             \
+    hipLaunchKernelGGL((k_p_spmm_mfma<T>), dim3((unsigned)grid), dim3(256), 0, stream,             \
+                       (const T *)values, index, (const T *)X, ldx, (T *)Y, ldy, L->M, N, L->n,    \
+                       L->m, L->g, L->P, L->S, L->B, row_tiles, tok_tiles, xvec)
+        if (L->dtype == NMG_F32) NMG_P_MFMA(float);
+        else NMG_P_MFMA(_Float16);
+#undef NMG_P_MFMA
+        return launched();
+    }
+    if (kernel != NMG_KERNEL_VALU) return NMG_ERR_UNSUPPORTED;
     const int tok_tiles = (N + kPTokens - 1) / kPTokens;
     const int64_t grid = (int64_t)(L->M / L->S) * tok_tiles;
     if (grid > INT32_MAX) return NMG_ERR_PARAM;
     const int waves = (L->S + kPRowsWave - 1) / kPRowsWave;
-    // binary32 X rows on 16-byte boundaries are read 4 tokens at a time
-    const size_t es = elem_size(L->dtype);
-    const bool xvec = aligned(X, 4 * es) && ldx % 4 == 0;
     // staging pays when the chunk has enough rows (4 waves or more) to share
     // each staged row; small chunks gather (measured on the 3072 x 768 sweep)
     const bool staged = L->m <= kPStageRows && L->S >= 64;

@@ -345,12 +345,17 @@ __global__ __launch_bounds__(kBlock) void k_repack(
 
 namespace nmg_internal {
 
+// whole 16-byte vectors: the rows, every chunk and the last chunk
+bool chunk_vec(const nmg_layout *L, const void *W, int64_t ldw) {
+    const int64_t es = L->dtype == NMG_F32 ? 4 : 2;
+    return aligned(W, 16) && (ldw * es) % 16 == 0 && (L->m * es) % 16 == 0 &&
+           (L->K * es) % 16 == 0;
+}
+
 template <typename T>
 nmg_status launch_compress_chunk(const nmg_layout *L, const void *W, int64_t ldw, void *values,
                                  uint8_t *indices, hipStream_t stream) {
-    // whole 16-byte vectors: the rows, every chunk and the last chunk
-    const bool vec = aligned(W, 16) && (ldw * sizeof(T)) % 16 == 0 &&
-                     (L->m * sizeof(T)) % 16 == 0 && (L->K * sizeof(T)) % 16 == 0;
+    const bool vec = chunk_vec(L, W, ldw);
     const int64_t pairs = (int64_t)(L->M / L->g) * L->C;
     const bool flat = pairs <= INT32_MAX - kBlock;
     const dim3 grid = flat ? dim3((unsigned)((pairs + kBlock - 1) / kBlock))
@@ -370,9 +375,13 @@ nmg_status launch_compress_chunk(const nmg_layout *L, const void *W, int64_t ldw
 nmg_status launch_compress(const nmg_layout *L, const void *W, int64_t ldw, void *values,
                            uint8_t *indices, hipStream_t stream) {
     // up to 32 columns per chunk and enough (group, chunk) pairs to fill the
-    // GPU: one thread per chunk, in registers; otherwise one thread per column
+    // GPU: one thread per chunk, in registers; otherwise one thread per column.
+    // Groups of at most 4 rows take the thread per chunk from 16K pairs, when
+    // its loads are vectors or at most 16 per row (a thread walks its rows in
+    // turn, so more rows favour a thread per column).
     const int64_t pairs = (int64_t)(L->M / L->g) * L->C;
-    if (L->m <= 32 && pairs >= 65536)
+    const bool few_rows = L->g <= 4 && pairs >= 16384 && (L->m <= 16 || chunk_vec(L, W, ldw));
+    if (L->m <= 32 && (pairs >= 65536 || few_rows))
         return L->dtype == NMG_F32
                    ? launch_compress_chunk<float>(L, W, ldw, values, indices, stream)
                    : launch_compress_chunk<_Float16>(L, W, ldw, values, indices, stream);

@@ -87,6 +87,7 @@ def lib():
         "nmg_p_layout_init": ([pp, i32, i32, i32, i32, i32, ctypes.c_int], ctypes.c_int),
         "nmg_p_compress": ([pp, vp, i64, vp, vp, vp], ctypes.c_int),
         "nmg_p_spmm": ([pp, vp, vp, vp, i64, i64, vp, i64, vp], ctypes.c_int),
+        "nmg_p_spmm_with": ([pp, ctypes.c_int, vp, vp, vp, i64, i64, vp, i64, vp], ctypes.c_int),
         "nmg_p_refine": ([pp, vp, i64, vp, vp, vp], ctypes.c_int),
         "nmg_p_densify": ([pp, vp, vp, vp, i64, vp], ctypes.c_int),
         "nmg_status_str": ([ctypes.c_int], ctypes.c_char_p),
@@ -354,16 +355,19 @@ def _p_check(layout: PLayout, values, index):
         raise ValueError(f"index must be contiguous {layout.index_shape}")
 
 
-def p_spmm(values, index, X, layout: PLayout):
-    """Y = W_s X for the chunked layout."""
+def p_spmm(values, index, X, layout: PLayout, kernel: str = "auto"):
+    """Y = W_s X for the chunked layout; kernel is "auto", "valu" or "mfma"."""
     _p_check(layout, values, index)
     _need_cuda(X)
     if X.dtype != layout.dtype or X.shape[0] != layout.K:
         raise ValueError("X must be K x N of the layout's dtype")
+    if kernel not in ("auto", "valu", "mfma"):
+        raise ValueError(f"unknown chunked-layout kernel {kernel!r}")
     Y = torch.empty((layout.M, X.shape[1]), dtype=X.dtype, device=X.device)
-    _check(lib().nmg_p_spmm(ctypes.byref(layout.c), _ptr(values), _ptr(index), _ptr(X),
-                            _rows(X, "X"), X.shape[1], _ptr(Y), _rows(Y, "Y"), _stream(X)),
-           "nmg_p_spmm")
+    _check(lib().nmg_p_spmm_with(ctypes.byref(layout.c), KERNELS[kernel], _ptr(values),
+                                 _ptr(index), _ptr(X), _rows(X, "X"), X.shape[1], _ptr(Y),
+                                 _rows(Y, "Y"), _stream(X)),
+           "nmg_p_spmm_with")
     return Y
 
 

@@ -160,6 +160,12 @@ def test_chunked_layout_validation(lib):
     assert lib.nmg_p_compress(ctypes.byref(L), None, 16, p, p, s) == nmg.ERR_NULL
     assert lib.nmg_p_compress(ctypes.byref(L), odd, 16, p, p, s) == nmg.ERR_ALIGN
     assert lib.nmg_p_spmm(ctypes.byref(L), p, p, p, 8, 16, p, 16, s) == nmg.ERR_PARAM  # ldx < N
+    assert lib.nmg_p_spmm_with(ctypes.byref(L), nmg.KERNELS["mfma_f16"], p, p, p, 16, 16, p, 16,
+                               s) == nmg.ERR_UNSUPPORTED   # not a chunked-layout kernel
+    assert lib.nmg_p_spmm_with(ctypes.byref(L), nmg.KERNELS["mfma"], p, p, p, 8, 16, p, 16,
+                               s) == nmg.ERR_PARAM          # ldx < N
+    assert lib.nmg_p_spmm_with(ctypes.byref(L), nmg.KERNELS["valu"], p, p, None, 16, 16, p, 16,
+                               s) == nmg.ERR_NULL
     assert lib.nmg_p_densify(ctypes.byref(L), p, None, p, 16, s) == nmg.ERR_NULL
     assert lib.nmg_p_refine(ctypes.byref(L), p, 8, p, p, s) == nmg.ERR_PARAM       # ldw < K
     assert lib.nmg_p_refine(ctypes.byref(L), p, 16, p, None, s) == nmg.ERR_NULL

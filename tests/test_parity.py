@@ -568,10 +568,15 @@ def test_chunked_layout(nmg, M, K, N, n, m, g, dtype):
     dense = nmg.p_densify(v, idx, L)
     rd, _ = oracle.p_densify(rv, ridx, K, n, m, g)
     assert np.array_equal(bits(np_of(dense)), bits(rd))
-    Y = nmg.p_spmm(v, idx, X.to(DEV), L)
-    torch.cuda.synchronize()
     Yref, B = oracle.p_spmm(rv, ridx, np_of(X), K, n, m, g)
-    check_product(Y, Yref, B, dtype, "chunked")
+    Xd = X.to(DEV)
+    for kernel in ("auto", "valu", "mfma"):
+        if kernel == "mfma" and m > 32:
+            continue
+        print(f"[chunked spmm] {kernel}", flush=True)
+        Y = nmg.p_spmm(v, idx, Xd, L, kernel)
+        torch.cuda.synchronize()
+        check_product(Y, Yref, B, dtype, f"chunked {kernel}")
 
 
 def random_chunked(count=30, seed=2305):
@@ -650,14 +655,17 @@ def test_chunked_layout_ffn_shape(nmg):
     torch.cuda.synchronize()
     rv, ridx = oracle.p_compress(np_of(W), 1, 4, 8)
     assert np.array_equal(np_of(idx), ridx) and np.array_equal(bits(np_of(v)), bits(rv))
-    Y = nmg.p_spmm(v, idx, X.to(DEV), L)
-    torch.cuda.synchronize()
     rd, _ = oracle.p_densify(rv, ridx, lin.K, 1, 4, 8)
     rows = np.random.default_rng(9).choice(lin.M, 192, replace=False)
     Xd = np_of(X).astype(np.float64)
     Yref = rd[rows].astype(np.float64) @ Xd
     B = np.abs(rd[rows].astype(np.float64)) @ np.abs(Xd)
-    check_product(Y[torch.as_tensor(rows, device=Y.device)], Yref, B, torch.float32, "chunked ffn")
+    for kernel in ("valu", "mfma"):
+        print(f"[chunked ffn] {kernel}", flush=True)
+        Y = nmg.p_spmm(v, idx, X.to(DEV), L, kernel)
+        torch.cuda.synchronize()
+        check_product(Y[torch.as_tensor(rows, device=Y.device)], Yref, B, torch.float32,
+                      f"chunked ffn {kernel}")
 
 
 
