@@ -534,8 +534,25 @@ constexpr int kPmKw = 32;                 // k columns per window, at most
 constexpr int kPmLda = kPmRows + 16;      // padded leading dimensions: the 4 k
 constexpr int kPmLdb = kPmTok + 16;       // rows of an operand read fall on 4
                                           // disjoint sets of 16 banks
+constexpr int kPmPre = 8;                 // kept weights prefetched per thread and window
 
-template <typename T>
+// Division of e < 2^16 by 1 <= d < 2^16 through a multiply-high: with
+// mul = ceil(2^32 / d), floor(e mul / 2^32) = floor(e / d) since e d < 2^32.
+__device__ __forceinline__ uint32_t magic_u16(uint32_t d) {
+    return d > 1 ? (uint32_t)(0xffffffffu / d + 1u) : 0u;
+}
+__device__ __forceinline__ uint32_t div_u16(uint32_t e, uint32_t mul, uint32_t d) {
+    return d > 1 ? __umulhi(e, mul) : e;
+}
+
+// N4 > 0: m = 4 and n = N4 <= 3 with whole windows (B % 8 == 0), values on
+// 16-byte and the index on 4-byte boundaries, and at most 256 stored rows per
+// tile: thread j owns stored row j of the tile's chunks for the whole K loop
+// (its chunk slot, target rows and pattern fixed), loads its window of kept
+// weights as 16-byte vectors and its 8 index bytes as 2 words, and scatters
+// them with register indices known at compile time.  N4 = 0: any m <= 32,
+// element by element.
+template <typename T, int N4>
 __global__ __launch_bounds__(256) void k_p_spmm_mfma(const T *__restrict__ values,
                                                      const uint8_t *__restrict__ index,
                                                      const T *__restrict__ X, int64_t ldx,
@@ -568,59 +585,126 @@ __global__ __launch_bounds__(256) void k_p_spmm_mfma(const T *__restrict__ value
         for (int j = 0; j < 4; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
     const int nbw = kPmKw / m;   // block columns per window (m <= kPmKw, host checked)
-    for (int b0 = 0; b0 < B; b0 += nbw) {
-        const int nb = min(nbw, B - b0);
-        const int kw = nb * m, kw4 = (kw + 3) & ~3;
-        // X rows b0 m .. b0 m + kw - 1 of this token tile into registers first
-        // (rows past kw re-read row kw - 1 and are stored as zeros), so the
-        // loads are in flight together
-        v4f xr[kPmKw / 4];
-        const int kx = tid >> 6, tx = t0 + 4 * lane;
+    // A window's kept weights: ns stored rows x nb * n values, element e of
+    // stored row e / (nb n).  Thread tid prefetches elements tid + 256 q
+    // (q < kPmPre) and their index bytes into registers while the previous
+    // window is multiplied; elements past 256 kPmPre are read when scattered.
+    // (kept in their loaded types, converted where they are written to LDS,
+    // so that nothing waits for them before the multiplications)
+    const int kx = tid >> 6, tx = t0 + 4 * lane;
+    typedef typename std::conditional<std::is_same<T, float>::value, v4f, h4>::type XV;
+    XV xr[kPmKw / 4];
+    constexpr int kRowPre = N4 > 0 ? 1 : kPmPre;   // element path only
+    T pv[kRowPre];
+    uint8_t pi[kRowPre];
+    // row path: this thread's stored row, its vectors and index words
+    typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+    constexpr int kRowVec = N4 > 0 ? 8 * N4 * (int)sizeof(T) / 16 : 1;
+    u4 rv[kRowVec];
+    uint32_t ri[2];
+    const int jrow = min(tid, ns - 1);
+    const T *vrow = values + (int64_t)(s_lo + jrow) * ldv;
+    const uint8_t *irow = index + (int64_t)(s_lo + jrow) * B;
+    const int jslot = jrow % S;
+    const int rbase = s_lo + jrow - jslot - R0;   // tile row of chunk row 0
+    auto prefetch = [&](int b0) {
+        const int nb = min(nbw, B - b0), kw = nb * m, nvw = nb * n, total = ns * nvw;
+        const uint32_t mv = magic_u16(nvw), mn = magic_u16(n);
 #pragma unroll
         for (int q = 0; q < kPmKw / 4; ++q) {
+            // rows past kw re-read row kw - 1 (stored as zeros)
             const int k = min(kx + 4 * q, kw - 1);
             const T *src = X + ((int64_t)b0 * m + k) * ldx + tx;
             if (xfull) {
-                if constexpr (std::is_same<T, float>::value) {
-                    xr[q] = *reinterpret_cast<const v4f *>(src);
-                } else {
-                    const h4 h = *reinterpret_cast<const h4 *>(src);
-                    xr[q] = v4f{(float)h[0], (float)h[1], (float)h[2], (float)h[3]};
-                }
+                xr[q] = *reinterpret_cast<const XV *>(src);
             } else {
-                xr[q] = load4<T>(src, N - tx, xvec);
+                const v4f x = load4<T>(src, N - tx, xvec);   // binary16 back exactly
+                xr[q] = XV{(T)x[0], (T)x[1], (T)x[2], (T)x[3]};
             }
         }
+        if constexpr (N4 > 0) {
+            (void)total;
+#pragma unroll
+            for (int q = 0; q < kRowVec; ++q)
+                rv[q] = *reinterpret_cast<const u4 *>(vrow + (int64_t)b0 * N4 + q * (16 / (int)sizeof(T)));
+            ri[0] = *reinterpret_cast<const uint32_t *>(irow + b0);
+            ri[1] = *reinterpret_cast<const uint32_t *>(irow + b0 + 4);
+            return;
+        }
+#pragma unroll
+        for (int q = 0; q < kRowPre; ++q) {
+            const uint32_t e = (uint32_t)min(tid + 256 * q, total - 1);   // clamped: in bounds
+            const uint32_t j = div_u16(e, mv, nvw), qq = e - j * nvw;
+            const uint32_t w = div_u16(qq, mn, n);
+            const int64_t Rs = s_lo + (int64_t)j;
+            pv[q] = values[Rs * ldv + (int64_t)b0 * n + qq];
+            pi[q] = index[Rs * B + b0 + w];
+        }
+    };
+    prefetch(0);
+    for (int b0 = 0; b0 < B; b0 += nbw) {
+        const int nb = min(nbw, B - b0);
+        const int kw = nb * m, kw4 = (kw + 3) & ~3;
+        const int nvw = nb * n, total = ns * nvw;
+        const uint32_t mv = magic_u16(nvw), mn = magic_u16(n), mg = magic_u16(g),
+                       ms = magic_u16(S);
         __syncthreads();  // the previous window is no longer read
-        // A: every stored block of the tile's chunks writes its expanded m
-        // values at its chunk row; k columns kw .. kw4 - 1 are zero
-        for (int i = tid; i < (kw4 - kw) * kPmRows; i += 256)
-            As[(kw + i / kPmRows) * kPmLda + i % kPmRows] = 0.f;
-        for (int i = tid; i < ns * nb; i += 256) {
-            const int j = i / nb, w = i - j * nb;
-            const int Rs = s_lo + j;                         // stored row
-            const int js = Rs % S;                           // its slot in the chunk
-            const int rho = min((int)index[(int64_t)Rs * B + b0 + w], S - 1);  // clamped
-            const int r = Rs - js + rho - R0;                // its row in the tile
-            if (r < 0 || r >= kPmRows) continue;
-            const uint8_t *off = pat + (js / g) * n;
-            const T *v = values + (int64_t)Rs * ldv + (int64_t)(b0 + w) * n;
-            float *a = As + (w * m) * kPmLda + r;
-            int s = 0;
-            for (int k = 0; k < m; ++k) {
-                float x = 0.f;
-                if (s < n && off[s] == k) x = (float)v[s++];
-                a[k * kPmLda] = x;
-            }
+        // A's k columns 0 .. kw4 - 1 to zero; X rows into B (rows kw .. kw4 - 1 zero)
+        for (int i = tid; i < kw4 * (kPmRows / 4); i += 256) {
+            const int k = i / (kPmRows / 4), c4 = i % (kPmRows / 4);
+            *reinterpret_cast<v4f *>(As + k * kPmLda + 4 * c4) = v4f{0.f, 0.f, 0.f, 0.f};
         }
 #pragma unroll
         for (int q = 0; q < kPmKw / 4; ++q) {
             const int k = kx + 4 * q;
-            if (k < kw4)
+            if (k < kw4) {
+                const v4f x = v4f{(float)xr[q][0], (float)xr[q][1], (float)xr[q][2], (float)xr[q][3]};
                 *reinterpret_cast<v4f *>(Bs + k * kPmLdb + 4 * lane) =
-                    k < kw ? xr[q] : v4f{0.f, 0.f, 0.f, 0.f};
+                    k < kw ? x : v4f{0.f, 0.f, 0.f, 0.f};
+            }
         }
         __syncthreads();
+        // every kept weight to its chunk row (A[w m + offset][row])
+        auto scatter = [&](uint32_t e, float v, int rho) {
+            const uint32_t j = div_u16(e, mv, nvw), qq = e - j * nvw;
+            const uint32_t w = div_u16(qq, mn, n), sl = qq - w * n;
+            const uint32_t js = j - div_u16(j, ms, S) * S;             // slot in the chunk
+            const int r = s_lo + (int)(j - js) + min(rho, S - 1) - R0;  // row in the tile
+            if (r >= 0 && r < kPmRows)
+                As[(w * m + pat[div_u16(js, mg, g) * n + sl]) * kPmLda + r] = v;
+        };
+        if constexpr (N4 > 0) {
+            if (tid < ns) {
+                const T *vals = reinterpret_cast<const T *>(rv);
+                const uint8_t *off = pat + (jslot / g) * N4;
+                int o[N4];
+#pragma unroll
+                for (int sl = 0; sl < N4; ++sl) o[sl] = off[sl];
+#pragma unroll
+                for (int w = 0; w < 8; ++w) {
+                    const int rho = (ri[w >> 2] >> (8 * (w & 3))) & 0xff;
+                    const int r = rbase + min(rho, S - 1);
+                    if ((unsigned)r < (unsigned)kPmRows)
+#pragma unroll
+                        for (int sl = 0; sl < N4; ++sl)
+                            As[(4 * w + o[sl]) * kPmLda + r] = (float)vals[w * N4 + sl];
+                }
+            }
+        } else {
+#pragma unroll
+        for (int q = 0; q < kRowPre; ++q) {
+            const int e = tid + 256 * q;
+            if (e < total) scatter((uint32_t)e, (float)pv[q], (int)pi[q]);
+        }
+        }
+        for (int e = tid + 256 * kRowPre; N4 == 0 && e < total; e += 256) {
+            const uint32_t j = div_u16((uint32_t)e, mv, nvw), qq = (uint32_t)e - j * nvw;
+            const int64_t Rs = s_lo + (int64_t)j;
+            scatter((uint32_t)e, (float)values[Rs * ldv + (int64_t)b0 * n + qq],
+                    index[Rs * B + b0 + div_u16(qq, mn, n)]);
+        }
+        __syncthreads();
+        if (b0 + nbw < B) prefetch(b0 + nbw);
         // 16 x 16 x 4 steps: lane (lr, lk) brings A[row lr][k lk] and
         // B[k lk][token lr]; row tiles i and token tiles j of this wave
         for (int k0 = 0; k0 < kw4; k0 += 4) {
@@ -756,12 +840,29 @@ nmg_status launch_p_spmm(const nmg_p_layout *L, nmg_kernel kernel, const void *v
         const int tok_tiles = (N + kPmTok - 1) / kPmTok;
         const int64_t grid = (int64_t)row_tiles * tok_tiles;
         if (grid > INT32_MAX) return NMG_ERR_PARAM;
-#define NMG_P_MFMA(T)                                                                             \
-    hipLaunchKernelGGL((k_p_spmm_mfma<T>), dim3((unsigned)grid), dim3(256), 0, stream,             \
+        // the row path (see k_p_spmm_mfma): m = 4, whole windows, aligned
+        // rows, and a tile's chunks hold at most 256 stored rows (S <= 128, or
+        // tiles that never straddle two chunks)
+        const bool rows = L->m == 4 && L->n <= 3 && L->B % 8 == 0 && aligned(values, 16) &&
+                          aligned(index, 4) && (L->S <= 128 || L->S % kPmRows == 0);
+        const int n4 = rows ? L->n : 0;
+#define NMG_P_MFMA(T, N4)                                                                         \
+    hipLaunchKernelGGL((k_p_spmm_mfma<T, N4>), dim3((unsigned)grid), dim3(256), 0, stream,         \
                        (const T *)values, index, (const T *)X, ldx, (T *)Y, ldy, L->M, N, L->n,    \
                        L->m, L->g, L->P, L->S, L->B, row_tiles, tok_tiles, xvec)
-        if (L->dtype == NMG_F32) NMG_P_MFMA(float);
-        else NMG_P_MFMA(_Float16);
+#define NMG_P_MFMA_N(T)                                                                           \
+    switch (n4) {                                                                                 \
+        case 1: NMG_P_MFMA(T, 1); break;                                                          \
+        case 2: NMG_P_MFMA(T, 2); break;                                                          \
+        case 3: NMG_P_MFMA(T, 3); break;                                                          \
+        default: NMG_P_MFMA(T, 0); break;                                                         \
+    }
+        if (L->dtype == NMG_F32) {
+            NMG_P_MFMA_N(float);
+        } else {
+            NMG_P_MFMA_N(_Float16);
+        }
+#undef NMG_P_MFMA_N
 #undef NMG_P_MFMA
         return launched();
     }

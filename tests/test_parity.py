@@ -550,6 +550,10 @@ P_SHAPES = [
     (256, 32, 40, 1, 4, 64, torch.float16),     # S = 256, one chunk row-set
     (224, 16, 33, 2, 8, 8, torch.float32),      # 28 patterns, S = 224
     (768, 768, 128, 2, 4, 4, torch.float32),    # the single-layer shape
+    # m = 4 with whole 8-block windows: the matrix-core kernel's row path
+    (96, 64, 300, 3, 4, 8, torch.float32),      # n = 3, ragged N
+    (192, 64, 70, 2, 4, 16, torch.float16),     # S = 96: tiles straddle two chunks
+    (384, 128, 513, 1, 4, 48, torch.float32),   # S = 192, N past a whole tile
 ]
 
 
