@@ -12,13 +12,13 @@
 //                 lower row) -- the same pairs, in the same order, as scanning
 //                 the sorted list of all pairs, since a pair that is not
 //                 eligible never becomes eligible again.
-//   k_p_compress_w the same greedy for chunks of at most 1024 (row, pattern)
-//                 pairs: one wave per chunk, each lane holding up to 16 pairs'
+//   k_p_compress_w the same greedy for chunks of at most 1536 (row, pattern)
+//                 pairs: one wave per chunk, each lane holding up to 24 pairs'
 //                 keys in registers with a mask of the pairs still eligible;
 //                 every step is a wave-wide maximum by shuffles, the pattern
 //                 counts live in registers (pattern p with lane p % 64), so a
-//                 workgroup of 4 waves converts 4 chunks with 28 KB of LDS.
-//   k_p_refine_w  the same swap search for chunks of at most 1024 pairs: one
+//                 workgroup of 4 waves converts 4 chunks with 24 KB of LDS.
+//   k_p_refine_w  the same swap search for chunks of at most 1536 pairs: one
 //                 wave per chunk, each lane owning up to 4 rows, the round's
 //                 flag a wave vote.
 //   k_p_spmm      vector FMAs: the rows of a group are scattered over the
@@ -165,7 +165,7 @@ __global__ __launch_bounds__(kBlock) void k_p_compress(const T *__restrict__ W, 
 // One wave per chunk, for chunks of at most kPwPairs * 64 pairs (see the
 // file comment); the same keys, eligibility and order as k_p_compress.
 constexpr int kPwWaves = 4;
-constexpr int kPwPairs = 16;       // pairs per lane
+constexpr int kPwPairs = 24;       // pairs per lane, at most (the live mask is 32 bits)
 constexpr int kPwWblk = 1024;      // S * m weights per chunk
 constexpr int kPwPat = 1024;       // P * n pattern offsets per chunk
 
@@ -176,7 +176,9 @@ __device__ __forceinline__ void p_wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <typename T>
+// PP pairs per lane (16 for chunks of up to 1024 pairs, else kPwPairs: every
+// step scans all PP, so small chunks take the smaller PP).
+template <typename T, int PP>
 __global__ __launch_bounds__(64 * kPwWaves) void k_p_compress_w(const T *__restrict__ W, int64_t ldw,
                                                                 T *__restrict__ values,
                                                                 uint8_t *__restrict__ index, int n,
@@ -201,11 +203,11 @@ __global__ __launch_bounds__(64 * kPwWaves) void k_p_compress_w(const T *__restr
     p_wave_sync();
 
     // this lane's pairs j = lane + 64 q: key as in k_p_compress, row and pattern
-    unsigned long long key[kPwPairs];
-    uint32_t rp[kPwPairs];
+    unsigned long long key[PP];
+    uint32_t rp[PP];
     uint32_t alive = 0;
 #pragma unroll
-    for (int q = 0; q < kPwPairs; ++q) {
+    for (int q = 0; q < PP; ++q) {
         const int j = lane + 64 * q;
         key[q] = 0;
         rp[q] = 0xffffu;
@@ -225,7 +227,7 @@ __global__ __launch_bounds__(64 * kPwWaves) void k_p_compress_w(const T *__restr
     for (int it = 0; it < S; ++it) {
         unsigned long long k = 0;
 #pragma unroll
-        for (int q = 0; q < kPwPairs; ++q)
+        for (int q = 0; q < PP; ++q)
             if ((alive >> q) & 1u) k = max(k, key[q]);
         for (int off = 32; off > 0; off >>= 1) k = max(k, (unsigned long long)__shfl_xor(k, off));
         // every step has a pair: the free rows equal the free pattern places
@@ -243,7 +245,7 @@ __global__ __launch_bounds__(64 * kPwWaves) void k_p_compress_w(const T *__restr
         if (lane == 0) assigned[rw] = pw;
         const bool full = now >= g;
 #pragma unroll
-        for (int q = 0; q < kPwPairs; ++q) {
+        for (int q = 0; q < PP; ++q) {
             const uint32_t r = rp[q] >> 8, p = rp[q] & 0xffu;
             if (r == (uint32_t)rw || (full && p == (uint32_t)pw)) alive &= ~(1u << q);
         }
@@ -760,14 +762,19 @@ nmg_status launch_p_compress(const nmg_p_layout *L, const void *W, int64_t ldw, 
     if (L->S * L->P <= 64 * kPwPairs && L->S * L->m <= kPwWblk && L->P * L->n <= kPwPat &&
         chunks <= INT32_MAX - kPwWaves) {
         const unsigned blocks = (unsigned)((chunks + kPwWaves - 1) / kPwWaves);
-        if (L->dtype == NMG_F32)
-            hipLaunchKernelGGL((k_p_compress_w<float>), dim3(blocks), dim3(64 * kPwWaves), 0, stream,
-                               (const float *)W, ldw, (float *)values, index, L->n, L->m, L->g,
-                               L->P, L->S, L->B, (int)chunks);
-        else
-            hipLaunchKernelGGL((k_p_compress_w<_Float16>), dim3(blocks), dim3(64 * kPwWaves), 0,
-                               stream, (const _Float16 *)W, ldw, (_Float16 *)values, index, L->n,
-                               L->m, L->g, L->P, L->S, L->B, (int)chunks);
+        const bool small = L->S * L->P <= 64 * 16;
+#define NMG_P_W(T, PP)                                                                            \
+    hipLaunchKernelGGL((k_p_compress_w<T, PP>), dim3(blocks), dim3(64 * kPwWaves), 0, stream,      \
+                       (const T *)W, ldw, (T *)values, index, L->n, L->m, L->g, L->P, L->S, L->B,  \
+                       (int)chunks)
+        if (L->dtype == NMG_F32) {
+            if (small) NMG_P_W(float, 16);
+            else NMG_P_W(float, kPwPairs);
+        } else {
+            if (small) NMG_P_W(_Float16, 16);
+            else NMG_P_W(_Float16, kPwPairs);
+        }
+#undef NMG_P_W
         return launched();
     }
     dim3 grid(L->M / L->S, L->B);
