@@ -36,9 +36,10 @@
 //                 products are useful.  Each workgroup owns 64 rows x 256
 //                 tokens; per window of up to 32 k-columns every stored block
 //                 writes its expanded m values into a k-major LDS tile at its
-//                 chunk row (no inverse table), the X rows are staged in
-//                 binary32, and each wave runs 4 x 4 v_mfma_f32_16x16x4f32
-//                 tiles (64 rows x 64 tokens) over them.
+//                 chunk row (no inverse table), and each wave runs 4 x 4
+//                 v_mfma_f32_16x16x4f32 tiles (64 rows x 64 tokens) with its
+//                 X operands loaded from global memory straight into
+//                 registers, one window ahead.
 //   k_p_densify   one thread per stored block.
 //   k_p_refine    the swap search of the paper's GPU converter (Section 5.2),
 //                 in a fixed order: one workgroup per chunk, one thread per
@@ -533,9 +534,8 @@ bool p_fits(const nmg_p_layout *L) {
 constexpr int kPmRows = 64;               // rows per workgroup
 constexpr int kPmTok = 256;               // tokens per workgroup (64 per wave)
 constexpr int kPmKw = 32;                 // k columns per window, at most
-constexpr int kPmLda = kPmRows + 16;      // padded leading dimensions: the 4 k
-constexpr int kPmLdb = kPmTok + 16;       // rows of an operand read fall on 4
-                                          // disjoint sets of 16 banks
+constexpr int kPmLda = kPmRows + 16;      // padded: the 4 k rows of an A read
+                                          // fall on 4 disjoint sets of 16 banks
 constexpr int kPmPre = 8;                 // kept weights prefetched per thread and window
 
 // Division of e < 2^16 by 1 <= d < 2^16 through a multiply-high: with
@@ -554,8 +554,8 @@ __device__ __forceinline__ uint32_t div_u16(uint32_t e, uint32_t mul, uint32_t d
 // weights as 16-byte vectors and its 8 index bytes as 2 words, and scatters
 // them with register indices known at compile time.  N4 = 0: any m <= 32,
 // element by element.
-template <typename T, int N4>
-__global__ __launch_bounds__(256) void k_p_spmm_mfma(const T *__restrict__ values,
+template <typename T, int N4, bool XFULL>
+__global__ __launch_bounds__(256, 3) void k_p_spmm_mfma(const T *__restrict__ values,
                                                      const uint8_t *__restrict__ index,
                                                      const T *__restrict__ X, int64_t ldx,
                                                      T *__restrict__ Y, int64_t ldy, int M, int N,
@@ -563,7 +563,6 @@ __global__ __launch_bounds__(256) void k_p_spmm_mfma(const T *__restrict__ value
                                                      int row_tiles, int tok_tiles, bool xvec) {
     __shared__ uint8_t pat[kPMaxPat];
     __shared__ float As[kPmKw * kPmLda];   // expanded weights, As[k][row]
-    __shared__ float Bs[kPmKw * kPmLdb];   // X rows, Bs[k][token]
     const int tile = xcd_tile(blockIdx.x, row_tiles * tok_tiles);
     const int tt = tile / row_tiles, rt = tile - tt * row_tiles;
     const int R0 = rt * kPmRows, t0 = tt * kPmTok;
@@ -575,8 +574,8 @@ __global__ __launch_bounds__(256) void k_p_spmm_mfma(const T *__restrict__ value
     const int s_lo = (R0 / S) * S;
     const int s_hi = min(M, (min(M, R0 + kPmRows) + S - 1) / S * S);
     const int ns = s_hi - s_lo;
-    // whole 256-token tile of 16-byte aligned rows: vector loads, no tail
-    const bool xfull = xvec && t0 + kPmTok <= N;
+    // XFULL: every tile is 256 whole tokens of 16-byte aligned X rows (vector
+    // loads, no tail); otherwise each load is checked
 
     for (int p = tid; p < P; p += 256) p_unrank(m, n, p, pat + p * n);
 
@@ -593,9 +592,27 @@ __global__ __launch_bounds__(256) void k_p_spmm_mfma(const T *__restrict__ value
     // window is multiplied; elements past 256 kPmPre are read when scattered.
     // (kept in their loaded types, converted where they are written to LDS,
     // so that nothing waits for them before the multiplications)
-    const int kx = tid >> 6, tx = t0 + 4 * lane;
+    // X goes from global memory straight into the B operands: column c of this
+    // wave's token tile j is token t0 + 64 wave + 4 c + j, so lane (lr, lk)
+    // needs tokens 4 lr .. 4 lr + 3 of row k0 + lk for its 4 tiles -- one
+    // 16-byte load per k-step.  x[q] holds k-step q of the current window and
+    // is reloaded with k-step q of the next one as soon as it is read.
+    const int tx = t0 + 64 * wave + 4 * lr;
     typedef typename std::conditional<std::is_same<T, float>::value, v4f, h4>::type XV;
-    XV xr[kPmKw / 4];
+    XV x[kPmKw / 4];
+    auto load_x = [&](int b0, int q) {
+        // rows past kw re-read row kw - 1 (multiplied by zero weights and
+        // masked at use)
+        const int kw = min(nbw, B - b0) * m;
+        const int k = min(4 * q + lk, kw - 1);
+        const T *src = X + ((int64_t)b0 * m + k) * ldx + tx;
+        if constexpr (XFULL) {
+            x[q] = *reinterpret_cast<const XV *>(src);
+        } else {
+            const v4f v = load4<T>(src, N - tx, xvec);   // binary16 back exactly
+            x[q] = XV{(T)v[0], (T)v[1], (T)v[2], (T)v[3]};
+        }
+    };
     constexpr int kRowPre = N4 > 0 ? 1 : kPmPre;   // element path only
     T pv[kRowPre];
     uint8_t pi[kRowPre];
@@ -612,18 +629,6 @@ __global__ __launch_bounds__(256) void k_p_spmm_mfma(const T *__restrict__ value
     auto prefetch = [&](int b0) {
         const int nb = min(nbw, B - b0), kw = nb * m, nvw = nb * n, total = ns * nvw;
         const uint32_t mv = magic_u16(nvw), mn = magic_u16(n);
-#pragma unroll
-        for (int q = 0; q < kPmKw / 4; ++q) {
-            // rows past kw re-read row kw - 1 (stored as zeros)
-            const int k = min(kx + 4 * q, kw - 1);
-            const T *src = X + ((int64_t)b0 * m + k) * ldx + tx;
-            if (xfull) {
-                xr[q] = *reinterpret_cast<const XV *>(src);
-            } else {
-                const v4f x = load4<T>(src, N - tx, xvec);   // binary16 back exactly
-                xr[q] = XV{(T)x[0], (T)x[1], (T)x[2], (T)x[3]};
-            }
-        }
         if constexpr (N4 > 0) {
             (void)total;
 #pragma unroll
@@ -644,6 +649,9 @@ __global__ __launch_bounds__(256) void k_p_spmm_mfma(const T *__restrict__ value
         }
     };
     prefetch(0);
+#pragma unroll
+    for (int q = 0; q < kPmKw / 4; ++q) load_x(0, q);
+    const int b_last = (B - 1) / nbw * nbw;   // the last window's first block column
     for (int b0 = 0; b0 < B; b0 += nbw) {
         const int nb = min(nbw, B - b0);
         const int kw = nb * m, kw4 = (kw + 3) & ~3;
@@ -651,19 +659,10 @@ __global__ __launch_bounds__(256) void k_p_spmm_mfma(const T *__restrict__ value
         const uint32_t mv = magic_u16(nvw), mn = magic_u16(n), mg = magic_u16(g),
                        ms = magic_u16(S);
         __syncthreads();  // the previous window is no longer read
-        // A's k columns 0 .. kw4 - 1 to zero; X rows into B (rows kw .. kw4 - 1 zero)
+        // A's k columns 0 .. kw4 - 1 to zero
         for (int i = tid; i < kw4 * (kPmRows / 4); i += 256) {
             const int k = i / (kPmRows / 4), c4 = i % (kPmRows / 4);
             *reinterpret_cast<v4f *>(As + k * kPmLda + 4 * c4) = v4f{0.f, 0.f, 0.f, 0.f};
-        }
-#pragma unroll
-        for (int q = 0; q < kPmKw / 4; ++q) {
-            const int k = kx + 4 * q;
-            if (k < kw4) {
-                const v4f x = v4f{(float)xr[q][0], (float)xr[q][1], (float)xr[q][2], (float)xr[q][3]};
-                *reinterpret_cast<v4f *>(Bs + k * kPmLdb + 4 * lane) =
-                    k < kw ? x : v4f{0.f, 0.f, 0.f, 0.f};
-            }
         }
         __syncthreads();
         // every kept weight to its chunk row (A[w m + offset][row])
@@ -709,12 +708,17 @@ __global__ __launch_bounds__(256) void k_p_spmm_mfma(const T *__restrict__ value
         if (b0 + nbw < B) prefetch(b0 + nbw);
         // 16 x 16 x 4 steps: lane (lr, lk) brings A[row lr][k lk] and
         // B[k lk][token lr]; row tiles i and token tiles j of this wave
-        for (int k0 = 0; k0 < kw4; k0 += 4) {
-            float a[4], bx[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) a[i] = As[(k0 + lk) * kPmLda + 16 * i + lr];
+        for (int q = 0; q < kPmKw / 4; ++q) {
+            if (4 * q >= kw4) break;
+            float a[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) bx[j] = Bs[(k0 + lk) * kPmLdb + 64 * wave + 16 * j + lr];
+            for (int i = 0; i < 4; ++i) a[i] = As[(4 * q + lk) * kPmLda + 16 * i + lr];
+            const bool kin = 4 * q + lk < kw;   // padded k rows: zero operands
+            float bx[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) bx[j] = kin ? (float)x[q][j] : 0.f;
+            load_x(min(b0 + nbw, b_last), q);   // the last window reloads itself
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -722,18 +726,23 @@ __global__ __launch_bounds__(256) void k_p_spmm_mfma(const T *__restrict__ value
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i], bx[j], acc[i][j], 0, 0, 0);
         }
     }
-    // acc[i][j][e] = Y[R0 + 16 i + 4 lk + e][t0 + 64 wave + 16 j + lr]
+    // acc[i][j][e] = Y[R0 + 16 i + 4 lk + e][t0 + 64 wave + 4 lr + j]: the 4
+    // tiles give 4 consecutive tokens, one 16-byte store when whole
+    const bool yvec = XFULL && (uintptr_t)Y % (4 * sizeof(T)) == 0 && ldy % 4 == 0;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int row = R0 + 16 * i + 4 * lk + e;
             if (row >= M) continue;
-            T *y = Y + (int64_t)row * ldy;
+            T *y = Y + (int64_t)row * ldy + tx;
+            if (yvec) {
+                *reinterpret_cast<XV *>(y) =
+                    XV{(T)acc[i][0][e], (T)acc[i][1][e], (T)acc[i][2][e], (T)acc[i][3][e]};
+            } else {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int t = t0 + 64 * wave + 16 * j + lr;
-                if (t < N) y[t] = (T)acc[i][j][e];
+                for (int j = 0; j < 4; ++j)
+                    if (tx + j < N) y[j] = (T)acc[i][j][e];
             }
         }
 }
@@ -853,10 +862,17 @@ nmg_status launch_p_spmm(const nmg_p_layout *L, nmg_kernel kernel, const void *v
         const bool rows = L->m == 4 && L->n <= 3 && L->B % 8 == 0 && aligned(values, 16) &&
                           aligned(index, 4) && (L->S <= 128 || L->S % kPmRows == 0);
         const int n4 = rows ? L->n : 0;
+        // every token tile whole and X rows on 16-byte boundaries
+        const bool xfull = xvec && N % kPmTok == 0;
 #define NMG_P_MFMA(T, N4)                                                                         \
-    hipLaunchKernelGGL((k_p_spmm_mfma<T, N4>), dim3((unsigned)grid), dim3(256), 0, stream,         \
-                       (const T *)values, index, (const T *)X, ldx, (T *)Y, ldy, L->M, N, L->n,    \
-                       L->m, L->g, L->P, L->S, L->B, row_tiles, tok_tiles, xvec)
+    if (xfull)                                                                                    \
+        hipLaunchKernelGGL((k_p_spmm_mfma<T, N4, true>), dim3((unsigned)grid), dim3(256), 0,       \
+                           stream, (const T *)values, index, (const T *)X, ldx, (T *)Y, ldy, L->M, \
+                           N, L->n, L->m, L->g, L->P, L->S, L->B, row_tiles, tok_tiles, xvec);     \
+    else                                                                                          \
+        hipLaunchKernelGGL((k_p_spmm_mfma<T, N4, false>), dim3((unsigned)grid), dim3(256), 0,      \
+                           stream, (const T *)values, index, (const T *)X, ldx, (T *)Y, ldy, L->M, \
+                           N, L->n, L->m, L->g, L->P, L->S, L->B, row_tiles, tok_tiles, xvec)
 #define NMG_P_MFMA_N(T)                                                                           \
     switch (n4) {                                                                                 \
         case 1: NMG_P_MFMA(T, 1); break;                                                          \
