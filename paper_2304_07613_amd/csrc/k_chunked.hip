@@ -536,6 +536,8 @@ constexpr int kPmTok = 256;               // tokens per workgroup (64 per wave)
 constexpr int kPmKw = 32;                 // k columns per window, at most
 constexpr int kPmLda = kPmRows + 16;      // padded: the 4 k rows of an A read
                                           // fall on 4 disjoint sets of 16 banks
+constexpr int kPmLdr = kPmKw + 4;         // row path, A[row][k]: 16 rows' 16-byte
+                                          // reads cover the 256 bytes of banks once
 constexpr int kPmPre = 8;                 // kept weights prefetched per thread and window
 
 // Division of e < 2^16 by 1 <= d < 2^16 through a multiply-high: with
@@ -562,7 +564,8 @@ __global__ __launch_bounds__(256, 3) void k_p_spmm_mfma(const T *__restrict__ va
                                                      int n, int m, int g, int P, int S, int B,
                                                      int row_tiles, int tok_tiles, bool xvec) {
     __shared__ uint8_t pat[kPMaxPat];
-    __shared__ float As[kPmKw * kPmLda];   // expanded weights, As[k][row]
+    // expanded weights: As[k][row] (element path), As[row][k] (row path)
+    __shared__ __align__(16) float As[kPmKw * kPmLda];
     const int tile = xcd_tile(blockIdx.x, row_tiles * tok_tiles);
     const int tt = tile / row_tiles, rt = tile - tt * row_tiles;
     const int R0 = rt * kPmRows, t0 = tt * kPmTok;
@@ -604,7 +607,9 @@ __global__ __launch_bounds__(256, 3) void k_p_spmm_mfma(const T *__restrict__ va
         // rows past kw re-read row kw - 1 (multiplied by zero weights and
         // masked at use)
         const int kw = min(nbw, B - b0) * m;
-        const int k = min(4 * q + lk, kw - 1);
+        // k-step q of lane group lk: column 4 q + lk, or 8 lk + q on the row
+        // path (whole windows), where a lane's A values are then contiguous
+        const int k = N4 > 0 ? 8 * lk + q : min(4 * q + lk, kw - 1);
         const T *src = X + ((int64_t)b0 * m + k) * ldx + tx;
         if constexpr (XFULL) {
             x[q] = *reinterpret_cast<const XV *>(src);
@@ -659,12 +664,14 @@ __global__ __launch_bounds__(256, 3) void k_p_spmm_mfma(const T *__restrict__ va
         const uint32_t mv = magic_u16(nvw), mn = magic_u16(n), mg = magic_u16(g),
                        ms = magic_u16(S);
         __syncthreads();  // the previous window is no longer read
-        // A's k columns 0 .. kw4 - 1 to zero
-        for (int i = tid; i < kw4 * (kPmRows / 4); i += 256) {
-            const int k = i / (kPmRows / 4), c4 = i % (kPmRows / 4);
-            *reinterpret_cast<v4f *>(As + k * kPmLda + 4 * c4) = v4f{0.f, 0.f, 0.f, 0.f};
+        if constexpr (N4 == 0) {
+            // A's k columns 0 .. kw4 - 1 to zero
+            for (int i = tid; i < kw4 * (kPmRows / 4); i += 256) {
+                const int k = i / (kPmRows / 4), c4 = i % (kPmRows / 4);
+                *reinterpret_cast<v4f *>(As + k * kPmLda + 4 * c4) = v4f{0.f, 0.f, 0.f, 0.f};
+            }
+            __syncthreads();
         }
-        __syncthreads();
         // every kept weight to its chunk row (A[w m + offset][row])
         auto scatter = [&](uint32_t e, float v, int rho) {
             const uint32_t j = div_u16(e, mv, nvw), qq = e - j * nvw;
@@ -683,12 +690,18 @@ __global__ __launch_bounds__(256, 3) void k_p_spmm_mfma(const T *__restrict__ va
                 for (int sl = 0; sl < N4; ++sl) o[sl] = off[sl];
 #pragma unroll
                 for (int w = 0; w < 8; ++w) {
+                    // the whole block, zeros included: with a permutation index
+                    // every (row, block) of the tile is written once
                     const int rho = (ri[w >> 2] >> (8 * (w & 3))) & 0xff;
                     const int r = rbase + min(rho, S - 1);
-                    if ((unsigned)r < (unsigned)kPmRows)
+                    v4f blk = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
 #pragma unroll
                         for (int sl = 0; sl < N4; ++sl)
-                            As[(4 * w + o[sl]) * kPmLda + r] = (float)vals[w * N4 + sl];
+                            if (o[sl] == k) blk[k] = (float)vals[w * N4 + sl];
+                    if ((unsigned)r < (unsigned)kPmRows)
+                        *reinterpret_cast<v4f *>(As + r * kPmLdr + 4 * w) = blk;
                 }
             }
         } else {
@@ -708,13 +721,23 @@ __global__ __launch_bounds__(256, 3) void k_p_spmm_mfma(const T *__restrict__ va
         if (b0 + nbw < B) prefetch(b0 + nbw);
         // 16 x 16 x 4 steps: lane (lr, lk) brings A[row lr][k lk] and
         // B[k lk][token lr]; row tiles i and token tiles j of this wave
+        v4f ar[4];   // row path: A[16 i + lr][8 lk + 4 h .. + 3] for h = q / 4
 #pragma unroll
         for (int q = 0; q < kPmKw / 4; ++q) {
             if (4 * q >= kw4) break;
             float a[4];
+            if constexpr (N4 > 0) {
+                if (q % 4 == 0)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) a[i] = As[(4 * q + lk) * kPmLda + 16 * i + lr];
-            const bool kin = 4 * q + lk < kw;   // padded k rows: zero operands
+                    for (int i = 0; i < 4; ++i)
+                        ar[i] = *reinterpret_cast<const v4f *>(As + (16 * i + lr) * kPmLdr + 8 * lk + q);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) a[i] = ar[i][q % 4];
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) a[i] = As[(4 * q + lk) * kPmLda + 16 * i + lr];
+            }
+            const bool kin = N4 > 0 || 4 * q + lk < kw;   // padded k rows: zero operands
             float bx[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) bx[j] = kin ? (float)x[q][j] : 0.f;
