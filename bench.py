@@ -296,9 +296,9 @@ def cpu_baseline(args, lin, L, set0):
     t_probe = time.perf_counter() - t0
     rows = int(args.cpu_seconds / max(t_probe, 1e-6) * probe) // lin.g * lin.g
     rows = max(lin.g, min(lin.M, rows))
-    # repeat a short sample until about a second of work has been timed
+    # repeat the sample until the budget of CPU work has been timed
     reps, t_spmm = 0, 0.0
-    while reps == 0 or (t_spmm < 1.0 and reps < 20):
+    while reps == 0 or (t_spmm < args.cpu_seconds and reps < 1000):
         t0 = time.perf_counter()
         Yref, B = oracle.spmm(rv[:rows], ridx[:rows // lin.g], Xn, lin.K, lin.n, lin.m, lin.g,
                               cores)
