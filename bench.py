@@ -470,8 +470,8 @@ def copy_calibration(ctx, args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: this build "
-              f"runs on a single GPU (the product shards by tokens with no communication)",
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: the library "
+              f"has no multi-GPU path (the product would shard by tokens with no communication)",
               file=sys.stderr)
         sys.exit(2)
     ctx = Ctx()
