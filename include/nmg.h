@@ -39,7 +39,16 @@
  *     no pointer after a call returns and allocates no device memory.
  *   - Work is enqueued on `stream` (0 = the null stream) and runs
  *     asynchronously; a call returns after validation and launch.  Calls are
- *     thread-safe: the library has no mutable global state.
+ *     thread-safe.  The only mutable global state is two host-side caches of
+ *     HIP runtime queries that pick launch shapes: the compute-unit count per
+ *     device and the resident-workgroup count per (device, kernel, workgroup
+ *     size).  Each entry is filled on first use under a lock and never
+ *     changes afterwards, so a call's launch shape -- and with it the order
+ *     of its sums and its output bits -- depends only on its arguments and
+ *     the device, whichever thread makes it.
+ *   - Launch failures are read with hipGetLastError right after the launch;
+ *     an error that earlier runtime calls left pending on the calling thread
+ *     is cleared first (and not reported by this library).
  *   - Arguments are validated on the host before anything is launched; on an
  *     error nothing is enqueued and no output is written.
  *   - Floating-point inputs must be finite for the product; the selection is

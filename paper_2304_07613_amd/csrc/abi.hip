@@ -1,47 +1,81 @@
 // abi.hip -- the C ABI of libnmg (include/nmg.h): host-side validation and
 // dispatch to the kernels' launchers.  Nothing here touches the GPU except
-// through those launchers and two cached runtime queries.
+// through those launchers and two cached runtime queries (compute units per
+// device, occupancy per kernel and workgroup size).
 //
 // Paper: STen (arXiv 2304.07613), Section 5.
+#include <mutex>
+
 #include "common.hpp"
 
 namespace nmg_internal {
 
+namespace {
+// Per-device figures are cached for devices 0 .. kMaxDevices-1; others are
+// queried on every call.
+constexpr int kMaxDevices = 64;
+
+int current_device() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();  // leave no error pending for the next launch
+        return -1;
+    }
+    return dev;
+}
+}  // namespace
+
 int device_cus() {
-    static std::atomic<int> cus{0};
-    int v = cus.load(std::memory_order_relaxed);
-    if (v > 0) return v;
-    int dev = 0, c = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || c < 1)
+    static std::atomic<int> cus[kMaxDevices];  // 0 = not yet queried
+    const int dev = current_device();
+    if (dev >= 0 && dev < kMaxDevices) {
+        const int v = cus[dev].load(std::memory_order_relaxed);
+        if (v > 0) return v;
+    }
+    int c = 0;
+    if (dev < 0 || hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) !=
+                       hipSuccess || c < 1) {
+        (void)hipGetLastError();
         c = 256;
-    cus.store(c, std::memory_order_relaxed);
+    }
+    // every thread computes the same value for a device, so a plain store is
+    // race-free in effect
+    if (dev >= 0 && dev < kMaxDevices) cus[dev].store(c, std::memory_order_relaxed);
     return c;
 }
 
-// Occupancy figures from the HIP runtime, cached in a fixed table keyed by
-// (kernel, threads); a lost race only repeats the query.
+// Occupancy figures from the HIP runtime, cached per (device, kernel, threads)
+// in a table guarded by one mutex: an entry is written whole before any
+// thread can read it, so every caller sees either no entry or the complete
+// figure, and every call on a device gets the same launch shape.
 int kernel_occupancy(const void *kernel, int threads) {
     struct Entry {
-        std::atomic<const void *> kernel{nullptr};
-        std::atomic<int> threads{0};
-        std::atomic<int> occ{0};
+        const void *kernel;
+        int device, threads, occ;
     };
-    static Entry table[512];
-    const size_t h = ((reinterpret_cast<uintptr_t>(kernel) >> 4) * 31 + (size_t)threads) % 512;
-    Entry &e = table[h];
-    if (e.kernel.load(std::memory_order_acquire) == kernel &&
-        e.threads.load(std::memory_order_acquire) == threads) {
-        const int v = e.occ.load(std::memory_order_acquire);
-        if (v > 0) return v;
+    constexpr int kSlots = 512;
+    static std::mutex lock;
+    static Entry table[kSlots];
+    static int used = 0;
+    const int dev = current_device();
+    {
+        std::lock_guard<std::mutex> guard(lock);
+        for (int i = 0; i < used; ++i)
+            if (table[i].kernel == kernel && table[i].threads == threads &&
+                table[i].device == dev)
+                return table[i].occ;
     }
     int nb = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kernel, threads, 0) != hipSuccess || nb < 1)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kernel, threads, 0) != hipSuccess ||
+        nb < 1) {
+        (void)hipGetLastError();
         nb = 1;
-    e.occ.store(0, std::memory_order_release);
-    e.kernel.store(kernel, std::memory_order_release);
-    e.threads.store(threads, std::memory_order_release);
-    e.occ.store(nb, std::memory_order_release);
+    }
+    std::lock_guard<std::mutex> guard(lock);
+    for (int i = 0; i < used; ++i)  // another thread may have filled it meanwhile
+        if (table[i].kernel == kernel && table[i].threads == threads && table[i].device == dev)
+            return table[i].occ;
+    if (dev >= 0 && used < kSlots) table[used++] = Entry{kernel, dev, threads, nb};
     return nb;
 }
 
@@ -86,6 +120,7 @@ nmg_status nmg_compress(const nmg_layout *L, const void *W, int64_t ldw, void *v
     if (ldw < L->K) return NMG_ERR_PARAM;
     const size_t es = elem_size(L->dtype);
     if (!aligned(W, es) || !aligned(values, es)) return NMG_ERR_ALIGN;
+    prelaunch();
     return launch_compress(L, W, ldw, values, indices, stream);
 }
 
@@ -97,6 +132,7 @@ nmg_status nmg_repack(const nmg_layout *L, const void *W, int64_t ldw, const uin
     if (ldw < L->K) return NMG_ERR_PARAM;
     const size_t es = elem_size(L->dtype);
     if (!aligned(W, es) || !aligned(values, es)) return NMG_ERR_ALIGN;
+    prelaunch();
     return launch_repack(L, W, ldw, indices, values, stream);
 }
 
@@ -110,7 +146,7 @@ nmg_kernel nmg_spmm_auto_kernel(const nmg_layout *L, int64_t N) {
     }
     if (spmm_half_supported(L, nullptr, N, N)) return NMG_KERNEL_MFMA_F16;
     if (spmm_smfmac_supported(L, nullptr, nullptr, nullptr, N, N)) return NMG_KERNEL_SMFMAC_F16;
-    if (spmm_direct_preferred(L, N)) return NMG_KERNEL_MFMA_DIRECT;
+    if (spmm_direct_preferred(L, N, N)) return NMG_KERNEL_MFMA_DIRECT;
     if (spmm_scalar_supported(L, nullptr, N)) return NMG_KERNEL_MFMA_SCALAR;
     if (spmm_general_supported(L, N)) return NMG_KERNEL_MFMA_GENERAL;
     return spmm_valu_staged_preferred(L, nullptr, N, N) ? NMG_KERNEL_VALU_STAGED : NMG_KERNEL_VALU;
@@ -153,11 +189,12 @@ nmg_status nmg_spmm_epilogue(const nmg_layout *L, nmg_kernel kernel, nmg_epilogu
         dense.g = L->M;
         L = &dense;
     }
+    prelaunch();
     SpmmArgs a{L, values, indices, X, ldx, (int)N, Y, ldy, stream};
     const bool half_ok = spmm_half_supported(L, X, ldx, N);
     const bool scalar_ok = spmm_scalar_supported(L, indices, ldx);
     if (kernel == NMG_KERNEL_AUTO || kernel == NMG_KERNEL_MFMA) {
-        const bool direct = spmm_direct_preferred(L, N) && spmm_direct_supported(L, ldx);
+        const bool direct = spmm_direct_preferred(L, N, ldx);
         kernel = half_ok     ? NMG_KERNEL_MFMA_F16
                  : spmm_smfmac_supported(L, values, indices, X, ldx, N) ? NMG_KERNEL_SMFMAC_F16
                  : direct    ? NMG_KERNEL_MFMA_DIRECT
@@ -247,6 +284,7 @@ nmg_status nmg_p_compress(const nmg_p_layout *L, const void *W, int64_t ldw, voi
     if (ldw < L->K) return NMG_ERR_PARAM;
     const size_t es = elem_size(L->dtype);
     if (!aligned(W, es) || !aligned(values, es)) return NMG_ERR_ALIGN;
+    prelaunch();
     return launch_p_compress(L, W, ldw, values, index, stream);
 }
 
@@ -258,6 +296,7 @@ nmg_status nmg_p_refine(const nmg_p_layout *L, const void *W, int64_t ldw, void 
     if (ldw < L->K) return NMG_ERR_PARAM;
     const size_t es = elem_size(L->dtype);
     if (!aligned(W, es) || !aligned(values, es)) return NMG_ERR_ALIGN;
+    prelaunch();
     return launch_p_refine(L, W, ldw, values, index, stream);
 }
 
@@ -272,6 +311,7 @@ nmg_status nmg_p_spmm_with(const nmg_p_layout *L, nmg_kernel kernel, const void 
     if (N < 1 || N > INT32_MAX || ldx < N || ldy < N) return NMG_ERR_PARAM;
     const size_t es = elem_size(L->dtype);
     if (!aligned(X, es) || !aligned(values, es) || !aligned(Y, es)) return NMG_ERR_ALIGN;
+    prelaunch();
     return launch_p_spmm(L, kernel, values, index, X, ldx, (int)N, Y, ldy, stream);
 }
 
@@ -289,6 +329,7 @@ nmg_status nmg_p_densify(const nmg_p_layout *L, const void *values, const uint8_
     if (ldw < L->K) return NMG_ERR_PARAM;
     const size_t es = elem_size(L->dtype);
     if (!aligned(values, es) || !aligned(W_out, es)) return NMG_ERR_ALIGN;
+    prelaunch();
     return launch_p_densify(L, values, index, W_out, ldw, stream);
 }
 
@@ -306,6 +347,7 @@ nmg_status nmg_densify(const nmg_layout *L, const void *values, const uint8_t *i
     if (ldw < L->K) return NMG_ERR_PARAM;
     const size_t es = elem_size(L->dtype);
     if (!aligned(values, es) || !aligned(W_out, es)) return NMG_ERR_ALIGN;
+    prelaunch();
     return launch_densify(L, values, indices, W_out, ldw, stream);
 }
 
@@ -317,6 +359,7 @@ nmg_status nmg_gelu(nmg_dtype dtype, const void *in, void *out, int64_t count,
     if (count == 0) return NMG_OK;
     const size_t es = elem_size(dtype);
     if (!aligned(in, es) || !aligned(out, es)) return NMG_ERR_ALIGN;
+    prelaunch();
     return launch_gelu(dtype, in, out, count, stream);
 }
 
@@ -328,6 +371,7 @@ nmg_status nmg_add(nmg_dtype dtype, const void *a, const void *b, void *out, int
     if (count == 0) return NMG_OK;
     const size_t es = elem_size(dtype);
     if (!aligned(a, es) || !aligned(b, es) || !aligned(out, es)) return NMG_ERR_ALIGN;
+    prelaunch();
     return launch_add(dtype, a, b, out, count, stream);
 }
 

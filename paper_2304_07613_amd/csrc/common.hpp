@@ -39,6 +39,12 @@ inline bool x_vectorisable(const nmg_layout *L, const void *X, int64_t ldx) {
     return aligned(X, 4 * elem_size(L->dtype)) && ldx % 4 == 0;
 }
 
+// A launch's status is read right after it with hipGetLastError.  Each entry
+// point first clears whatever error earlier runtime calls on the thread left
+// pending (prelaunch), so that such an error is not reported as the failure
+// of this library's launch; the host queries the launchers make on the way
+// (device_cus, kernel_occupancy) clear their own errors.
+inline void prelaunch() { (void)hipGetLastError(); }
 inline nmg_status launched() {
     return hipGetLastError() == hipSuccess ? NMG_OK : NMG_ERR_LAUNCH;
 }
@@ -51,8 +57,9 @@ inline int mfma_unit(const nmg_layout *L) {
     return 0;
 }
 
-// Compute units of the current device (cached), and workgroups of `kernel`
-// with `threads` threads that fit one of them (cached per kernel and size).
+// Compute units of the current device (cached per device), and workgroups of
+// `kernel` with `threads` threads that fit one of its compute units (cached
+// per device, kernel and size).  Both are safe to call from any thread.
 int device_cus();
 int kernel_occupancy(const void *kernel, int threads);
 
@@ -100,7 +107,7 @@ nmg_status spmm_scalar_f32_u4(const SpmmArgs &a);
 nmg_status spmm_scalar_f16(const SpmmArgs &a);
 
 bool spmm_direct_supported(const nmg_layout *L, int64_t ldx);
-bool spmm_direct_preferred(const nmg_layout *L, int64_t N);
+bool spmm_direct_preferred(const nmg_layout *L, int64_t N, int64_t ldx);
 nmg_status spmm_direct(const SpmmArgs &a);
 
 bool spmm_smfmac_supported(const nmg_layout *L, const void *values, const uint8_t *indices,

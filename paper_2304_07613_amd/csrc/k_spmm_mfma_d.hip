@@ -363,8 +363,8 @@ nmg_status nmg_internal::spmm_direct(const SpmmArgs &a) {
 // unit of U rows reads its C * n selected rows.  Gathering wins when that
 // reads fewer bytes, and whenever the staged kernel would leave most CUs idle
 // (it has no k-split).
-bool nmg_internal::spmm_direct_preferred(const nmg_layout *L, int64_t N) {
-    if (!spmm_direct_supported(L, N)) return false;
+bool nmg_internal::spmm_direct_preferred(const nmg_layout *L, int64_t N, int64_t ldx) {
+    if (!spmm_direct_supported(L, ldx)) return false;
     const int64_t U = std::min(mfma_unit(L), 16);
     const int64_t ldv = (int64_t)L->C * L->n;
     if (128 * ldv <= U * L->K) return true;
