@@ -122,11 +122,22 @@ typedef enum nmg_kernel {
                                     gather; needs n in {1, 2}, m in {4, 8,
                                     16}, C * n % 8 == 0, values, indices, X and
                                     ldx on 16-byte boundaries, N % 8 == 0     */
-    NMG_KERNEL_VALU_STAGED = 8   /* vector-ALU FMA on X windows staged in LDS
+    NMG_KERNEL_VALU_STAGED = 8,  /* vector-ALU FMA on X windows staged in LDS
                                     (the choice for binary32 layouts the
                                     matrix-core kernels decline, g = 1 above
                                     all); needs binary32, m <= 32, n <= 16, X
                                     and ldx on 16-byte boundaries, N % 4 == 0 */
+    NMG_KERNEL_MFMA_WIDE = 9,    /* binary16 layouts on the 16 x 16 x 32
+                                    binary16 matrix instruction (32 gathered
+                                    k-slots of a group per instruction, binary32
+                                    accumulation); runs only through
+                                    nmg_spmm_x16 on prepared operands
+                                    (nmg_spmm_with returns
+                                    NMG_ERR_UNSUPPORTED)                      */
+    NMG_KERNEL_MFMA_SPLIT = 10   /* binary32 layouts on the same binary16
+                                    instruction, each operand carried as two
+                                    binary16 parts; runs only through
+                                    nmg_spmm_x16 (see there)                  */
 } nmg_kernel;
 /* With n == m every column is kept and every index row is 0 .. m-1, so the
  * matrix-core kernels treat the weight as one group whatever g is. */
@@ -201,6 +212,52 @@ nmg_status nmg_spmm_epilogue(const nmg_layout *layout, nmg_kernel kernel, nmg_ep
  * 16-byte aligned X, 4-byte aligned indices and ldx = N (never
  * NMG_KERNEL_MFMA; NMG_KERNEL_AUTO only for an invalid layout). */
 nmg_kernel nmg_spmm_auto_kernel(const nmg_layout *layout, int64_t N);
+
+/* ------------------------------------------------------------------------
+ * THE 16 x 16 x 32 PRODUCTS (Section 5.1's product on gfx950's
+ * v_mfma_f32_16x16x32_f16; families NMG_KERNEL_MFMA_WIDE and
+ * NMG_KERNEL_MFMA_SPLIT).  One instruction contracts 32 gathered k-slots of a
+ * group for 16 tokens; its per-window operands -- each lane's weight fragment
+ * and the in-chunk offsets of the X rows it reads -- are arranged once per
+ * packed weight ("prepared operands", a pure function of values and indices)
+ * and then reused by every product with that weight.
+ *
+ * Layouts taken: n in {1, 2}; g % 8 == 0; the staging of one window (32
+ * k-slots = 32 / n chunks of m X rows, 128 tokens per row) within the LDS
+ * buffers: binary16 needs m % 4 == 0 and (32 / n) (256 m + 32) <= 53248
+ * (m = 4 or 8 at n = 1, m <= 12 at n = 2); binary32 needs (32 / n) (512 m +
+ * 32) <= 81920 (m <= 4 at n = 1, m <= 9 at n = 2); M * C * n < 2^31.
+ *
+ * Binary32 (MFMA_SPLIT) is not binary32 arithmetic: every weight w (scaled by
+ * a power of two per 8 rows that puts the largest |w| of those rows into
+ * [2^13, 2^14)) and every X entry x is carried as hi = fp16(v), lo = fp16(v -
+ * hi), and all four products of the parts are summed in binary32; the
+ * output is scaled back exactly.  Per output, |Y - W_s X| is at most about
+ * 2^-20 B + 2^-25 sum_k |w_k| + (binary32 summation error), B = sum_k |w_k
+ * x_k| over the kept k, for finite X with |x| < 65504 -- within the 1e-5 B
+ * of the binary32 families whenever the kept X entries are not many orders
+ * of magnitude below 2^-5 on average.  NMG_KERNEL_AUTO never chooses it.
+ */
+
+/* Bytes of the prepared operands of a layout; -1 for an invalid layout or one
+ * these products do not take.  Pure host code. */
+int64_t nmg_x16_prepared_bytes(const nmg_layout *layout);
+
+/* Prepared operands from a packed weight (values, indices as nmg_compress
+ * writes them; binary16 layouts give MFMA_WIDE operands, binary32 MFMA_SPLIT
+ * operands).  `prepared` (device, 16-byte aligned, nmg_x16_prepared_bytes
+ * long) is written whole; values and indices are only read.
+ * NMG_ERR_UNSUPPORTED for a layout these products do not take. */
+nmg_status nmg_x16_prepare(const nmg_layout *layout, const void *values, const uint8_t *indices,
+                           void *prepared, hipStream_t stream);
+
+/* Y = W_s X from prepared operands.  X: K x N, leading dimension ldx; Y: M x
+ * N, leading dimension ldy; layout dtype for both.  Needs X and ldx on 16-byte
+ * boundaries, Y and ldy on 16-byte (binary32) / 8-byte (binary16) boundaries,
+ * N % 4 == 0 (binary32) / N % 8 == 0 (binary16), K * ldx < 2^31; else
+ * NMG_ERR_UNSUPPORTED. */
+nmg_status nmg_spmm_x16(const nmg_layout *layout, const void *prepared, const void *X,
+                        int64_t ldx, int64_t N, void *Y, int64_t ldy, hipStream_t stream);
 
 /* n:m:g -> dense (end of Section 5.2): W_out (M x K, leading dimension
  * ldw >= K) gets the kept weights at their columns and +0 elsewhere. */

@@ -339,6 +339,34 @@ nmg_status nmg_spmm(const nmg_layout *L, const void *values, const uint8_t *indi
     return nmg_spmm_with(L, NMG_KERNEL_AUTO, values, indices, X, ldx, N, Y, ldy, stream);
 }
 
+int64_t nmg_x16_prepared_bytes(const nmg_layout *L) {
+    if (check_layout(L) != NMG_OK) return -1;
+    return x16_prepared_bytes(L);
+}
+
+nmg_status nmg_x16_prepare(const nmg_layout *L, const void *values, const uint8_t *indices,
+                           void *prepared, hipStream_t stream) {
+    nmg_status st = check_layout(L);
+    if (st != NMG_OK) return st;
+    if (!values || !indices || !prepared) return NMG_ERR_NULL;
+    if (!x16_layout_supported(L)) return NMG_ERR_UNSUPPORTED;
+    if (!aligned(values, elem_size(L->dtype)) || !aligned(prepared, 16)) return NMG_ERR_ALIGN;
+    prelaunch();
+    return x16_prepare(L, values, indices, prepared, stream);
+}
+
+nmg_status nmg_spmm_x16(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
+                        int64_t N, void *Y, int64_t ldy, hipStream_t stream) {
+    nmg_status st = check_layout(L);
+    if (st != NMG_OK) return st;
+    if (!prepared || !X || !Y) return NMG_ERR_NULL;
+    if (N < 1 || N > INT32_MAX || ldx < N || ldy < N) return NMG_ERR_PARAM;
+    if (!aligned(prepared, 16)) return NMG_ERR_ALIGN;
+    if (!x16_args_supported(L, X, ldx, Y, ldy, N)) return NMG_ERR_UNSUPPORTED;
+    prelaunch();
+    return x16_product(L, prepared, X, ldx, (int)N, Y, ldy, stream);
+}
+
 nmg_status nmg_densify(const nmg_layout *L, const void *values, const uint8_t *indices,
                        void *W_out, int64_t ldw, hipStream_t stream) {
     nmg_status st = check_layout(L);

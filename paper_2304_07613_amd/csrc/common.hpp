@@ -116,6 +116,17 @@ nmg_status spmm_smfmac(const SpmmArgs &a);
 
 bool spmm_half_supported(const nmg_layout *L, const void *X, int64_t ldx, int64_t N);
 
+// the 16 x 16 x 32 products (k_spmm_x16.hip): layout and argument checks,
+// size of the prepared operands, preparation and product
+bool x16_layout_supported(const nmg_layout *L);
+bool x16_args_supported(const nmg_layout *L, const void *X, int64_t ldx, const void *Y,
+                        int64_t ldy, int64_t N);
+int64_t x16_prepared_bytes(const nmg_layout *L);
+nmg_status x16_prepare(const nmg_layout *L, const void *values, const uint8_t *indices,
+                       void *prepared, hipStream_t stream);
+nmg_status x16_product(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
+                       int N, void *Y, int64_t ldy, hipStream_t stream);
+
 nmg_status check_p_layout(const nmg_p_layout *L);
 int p_pattern_count(int m, int n);
 nmg_status launch_p_compress(const nmg_p_layout *L, const void *W, int64_t ldw, void *values,

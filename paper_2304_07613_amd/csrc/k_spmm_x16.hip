@@ -1,0 +1,731 @@
+// k_spmm_x16.hip -- the product Y = W_s X on the 16 x 16 x 32 binary16 matrix
+// instruction of gfx950 (v_mfma_f32_16x16x32_f16, binary32 accumulation), in
+// two modes:
+//
+//   HALF   binary16 layouts (binary16 in and out);
+//   SPLIT  binary32 layouts: every binary32 operand v is carried as two
+//          binary16 numbers, hi = fp16(v) and lo = fp16(v - hi) (for X the
+//          remainder scaled by 2^11, and the weights it meets scaled by 2^-11,
+//          so that it stays a normal number), and the four products hi*hi,
+//          hi*lo, lo*hi and lo*lo are all formed (exactly, in binary32) and
+//          summed in binary32.  hi + lo holds 22 of v's 24 significant bits,
+//          so each product is within about 2^-21 of the binary32 one; see
+//          nmg.h for the range in which this holds.
+//
+// Paper: STen (arXiv 2304.07613), Section 5.1 (the sparse x dense product of
+// the grouped n:m layout); the kernel itself is this library's design.
+//
+// Orientation.  One instruction computes D[t][j] += sum_k A[t][k] B[k][j] for
+// 16 tokens t, 16 columns j and 32 contraction indices k.  A holds gathered X
+// (a group's k-slots select the X rows, so the 32 k of one instruction are 32
+// k-slots of one group), B the group's weights; a column j is a weight row
+// (HALF: 16 rows of a group, or 8 with the other 8 columns zero), or in SPLIT
+// mode a (row, part) pair: columns 0-7 carry the hi parts of 8 rows, 8-15 the
+// lo parts, and one instruction reads the hi parts of X, a second one the lo
+// parts.  Lane l holds A[l % 16][8 (l / 16) + e] and B[8 (l / 16) + e][l % 16],
+// e = 0..7, and gets D[4 (l / 16) + i][l % 16], i = 0..3 (fitted to an
+// in-bounds probe of the instruction): 4 consecutive tokens of one row per
+// lane, a 16-byte store.
+//
+// Staging.  A workgroup covers R rows and a tile of 128 tokens; windows of 32
+// k-slots (32 / n whole chunks, all m X rows of each) are staged in LDS,
+// double-buffered, one barrier per window.  HALF copies X rows straight from
+// global memory into LDS; SPLIT loads binary32 X into registers, splits it and
+// writes a hi plane and a lo plane.  The A operand comes from two transposing
+// LDS reads (ds_read_b64_tr_b16): in each 16-lane group, lanes 4k .. 4k+3
+// read 16 tokens of the row of k-slot k, and lane i receives token i of the 4
+// rows side by side.
+//
+// LDS banks.  One transposing read touches 16 row segments of 32 bytes, and
+// each half-wave's 8 segments should fall on the 8 distinct 32-byte quarters
+// of the 256-byte bank window.  A row's in-chunk offset is data, so rows are
+// laid out with a stride that is a multiple of 256 bytes and chunks with a
+// stride of 32 bytes more: a segment's bank quarter depends only on its chunk
+// (and the token tile), and the order of k-slots inside a window (kb_slot)
+// puts 8 consecutive chunks in each half-wave's read.
+//
+// Scaling (SPLIT).  Each unit of 8 rows is multiplied by a power of two that
+// brings its largest |weight| into [2^13, 2^14), so the lo parts of its
+// weights are binary16 normal numbers whatever the weights' magnitude; the
+// output is multiplied back (exact).
+#include "common.hpp"
+
+namespace {
+
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef short s4 __attribute__((ext_vector_type(4)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+constexpr int kXSlots = 32;    // k-slots per window (one instruction's contraction)
+constexpr int kXTok = 128;     // tokens per tile
+constexpr int kXTiles = 8;     // 16-token sub-tiles per tile
+
+// The k-slot (0..31, within the window) that lane group q (= lane / 16) puts
+// at contraction index 8 q + e.  The transposing read r = e / 4 of half-wave h
+// = q / 2 reads the slots of "pass" P = 2 r + h: 8 slots from 8 consecutive
+// chunks (n <= 2), at pass position ps = 4 (q % 2) + e % 4.
+__host__ __device__ constexpr int kb_slot(int n, int q, int e) {
+    const int P = 2 * (e >> 2) + (q >> 1);
+    const int ps = 4 * (q & 1) + (e & 3);
+    const int cgroups = (kXSlots / n) / 8;  // groups of 8 chunks in a window
+    return (8 * (P % cgroups) + ps) * n + P / cgroups;
+}
+
+typedef __attribute__((address_space(3))) char lds_char;
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) u32x2 lds_u2;
+
+// The transposing LDS read of 8 bytes at `p`.
+__device__ __forceinline__ h4 lds_read_tr(lds_char *p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    return __builtin_bit_cast(h4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4 *)p));
+#else
+    (void)p;
+    return h4{};
+#endif
+}
+
+// s_waitcnt immediate: at most n vector-memory operations of this wave
+// outstanding, and (lgkm0) none of its LDS operations; expcnt left at its
+// maximum
+__host__ __device__ constexpr int waitcnt_imm(int n, bool lgkm0) {
+    return (n & 0xf) | ((n >> 4) << 14) | (0x7 << 4) | ((lgkm0 ? 0 : 0xf) << 8);
+}
+
+// The end of a window: this wave's copies into LDS up to `n` vector-memory
+// operations ago and all its LDS writes have landed (the waits are explicit:
+// a workgroup fence would also wait for the loads still in flight for later
+// windows, LDS copies counting as LDS writes), then the workgroup barrier; the
+// memory clobber keeps the compiler from moving LDS accesses across it.
+template <int n>
+__device__ __forceinline__ void window_barrier() {
+#if defined(__HIP_DEVICE_COMPILE__)
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(n, true));
+    asm volatile("s_barrier" ::: "memory");
+#endif
+}
+
+// a + (the value of lane l ^ 8 of the same 16-lane row)
+__device__ __forceinline__ float add_row_ror8(float a) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const int o = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, a), 0x128, 0xf, 0xf, false);
+    return a + __builtin_bit_cast(float, o);
+#else
+    return a;
+#endif
+}
+
+#ifndef X16_NT_STORE
+#define X16_NT_STORE 1
+#endif
+template <typename T>
+__device__ __forceinline__ void store_y(T v, T *p) {
+    if constexpr (X16_NT_STORE) __builtin_nontemporal_store(v, p);
+    else *p = v;
+}
+
+__device__ __forceinline__ uint32_t pack_h2(_Float16 lo, _Float16 hi) {
+    return (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+}
+
+// Workgroup geometry, shared by the kernel and its launcher.
+template <bool SPLIT, bool U16, int GW, int NW>
+struct XGeom {
+    static constexpr int rows_unit = SPLIT ? 8 : (U16 ? 16 : 8);
+    static constexpr int rows_wave = GW * rows_unit;
+    static constexpr int rows_wg = NW * rows_wave;
+    // bytes of one staged X row: SPLIT [hi 64 tokens | lo 64 tokens] twice,
+    // HALF 128 binary16 tokens
+    static constexpr int row_bytes = SPLIT ? 512 : 256;
+};
+
+// LDS bytes of one staging buffer (a multiple of 256)
+inline int x16_buffer_bytes(int n, int m, int row_bytes) {
+    const int cs = m * row_bytes + 32;
+    return ((kXSlots / n) * cs + 255) / 256 * 256;
+}
+// Staging buffers: binary16 three (window w + 2 is copied while w is
+// multiplied), binary32 two (its X passes through registers one window ahead)
+template <bool SPLIT> constexpr int x16_nbuf() { return SPLIT ? 2 : 3; }
+template <bool SPLIT> constexpr int x16_buf_cap() { return SPLIT ? 81920 : 53248; }
+
+// ---------------------------------------------------------------- prepared operands
+//
+// The product's per-window operands, computed once per packed weight: for
+// every unit of RU rows and window of 32 k-slots, each lane's B operand (8
+// binary16: the weights of its column at the slots kb_slot(q, 0..7), SPLIT
+// the hi or lo part of the scaled binary32 weight) and the in-chunk offsets
+// of the two rows its transposing reads fetch (the index bytes of slots
+// kb_slot(q, p / 4) and kb_slot(q, 4 + p / 4)); and per unit the exponent of
+// its scale (SPLIT).  Layout, for U units and W windows:
+//   frag   U * W * 64 entries of 16 bytes   [(unit * W + window) * 64 + lane]
+//   offs   U * W * 64 entries of 2 bytes    (low byte: read 0, high: read 1)
+//   scale  U bytes                          (signed exponent; 0 for binary16)
+struct XPrep {
+    int units, nwin;
+    size_t frag, offs, scale, bytes;  // byte offsets and total
+};
+inline XPrep x16_prep_layout(const nmg_layout *L, int ru) {
+    XPrep P;
+    P.units = L->M / ru;
+    P.nwin = (L->C * L->n + kXSlots - 1) / kXSlots;
+    const size_t e = (size_t)P.units * P.nwin * 64;
+    P.frag = 0;
+    P.offs = e * 16;
+    P.scale = P.offs + e * 2;
+    P.bytes = (P.scale + P.units + 255) / 256 * 256;
+    return P;
+}
+
+template <bool SPLIT, int NS, int RU>
+__global__ __launch_bounds__(64) void k_x16_prepare(const void *__restrict__ values_,
+                                                    const uint8_t *__restrict__ indices, h8 *frag,
+                                                    uint16_t *offs, int8_t *scale, int M, int m,
+                                                    int g, int C, int nwin) {
+    const int unit = blockIdx.x;
+    const int lane = threadIdx.x;
+    const int q = lane >> 4, p = lane & 15;
+    const int ldv = C * NS;
+    const int r0 = unit * RU;
+    const int grp = r0 / g;
+    // column -> row of the unit (SPLIT: row p % 8, part p / 8; binary16
+    // 8-row units: columns 8-15 are zero)
+    const int b_row = (SPLIT || RU == 16) ? (RU == 16 ? p : (p & 7)) : (p & 7);
+    const bool b_lo = SPLIT && p >= 8;
+    const bool b_zero = !SPLIT && RU == 8 && p >= 8;
+    int sc = 0;
+    if constexpr (SPLIT) {
+        // the unit's RU rows are contiguous: 8 independent loads per lane in flight
+        const float *vr = reinterpret_cast<const float *>(values_) + (int64_t)r0 * ldv;
+        const int nv = RU * ldv;
+        float mx = 0.f;
+        for (int i0 = 0; i0 < nv; i0 += 8 * 64) {
+            float x[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) x[k] = vr[min(i0 + k * 64 + lane, nv - 1)];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) mx = fmaxf(mx, fabsf(x[k]));
+        }
+#pragma unroll
+        for (int sh = 32; sh >= 1; sh >>= 1) mx = fmaxf(mx, __shfl_xor(mx, sh, 64));
+        if (mx > 0.f && mx <= 3.4e38f) {
+            int e = 0;
+            (void)frexpf(mx, &e);  // mx in [2^(e-1), 2^e): scaled max in [2^13, 2^14)
+            sc = 14 - e;
+        }
+        if (lane == 0) scale[unit] = (int8_t)sc;
+    } else {
+        if (lane == 0) scale[unit] = 0;
+    }
+    const float mul = __builtin_ldexpf(1.f, sc);
+    for (int win = 0; win < nwin; ++win) {
+        const int slot0 = win * kXSlots;
+        const size_t e0 = ((size_t)unit * nwin + win) * 64 + lane;
+        // A offsets
+        uint32_t oo = 0;
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            const int sl = slot0 + kb_slot(NS, q, 4 * r + (p >> 2));
+            const uint32_t o = sl < ldv ? min((uint32_t)indices[(int64_t)grp * ldv + sl], (uint32_t)(m - 1)) : 0u;
+            oo |= o << (8 * r);
+        }
+        offs[e0] = (uint16_t)oo;
+        // B operand
+        h8 b;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int sl = slot0 + kb_slot(NS, q, e);
+            _Float16 h = (_Float16)0.f;
+            if (sl < ldv && !b_zero) {
+                if constexpr (SPLIT) {
+                    const float w = reinterpret_cast<const float *>(values_)[(int64_t)(r0 + b_row) * ldv + sl] * mul;
+                    const _Float16 hi = (_Float16)w;
+                    const _Float16 lo = (_Float16)(w - (float)hi);
+                    h = b_lo ? lo : hi;
+                } else {
+                    h = reinterpret_cast<const _Float16 *>(values_)[(int64_t)(r0 + b_row) * ldv + sl];
+                }
+            }
+            b[e] = h;
+        }
+        frag[e0] = b;
+    }
+}
+
+// ---------------------------------------------------------------- the product
+
+template <bool SPLIT, int NS, bool U16, int GW, int NW, int NSTG>
+__global__ __launch_bounds__(64 * NW) void k_spmm_x16(
+    const h8 *__restrict__ frag, const uint16_t *__restrict__ offs, const int8_t *__restrict__ scale,
+    const void *__restrict__ X_, int64_t ldx, void *__restrict__ Y_, int64_t ldy, int M, int K,
+    int N, int m, int nwin, int row_blocks) {
+    using G = XGeom<SPLIT, U16, GW, NW>;
+    constexpr int RU = G::rows_unit, ROWB = G::row_bytes;
+    constexpr int CPW = kXSlots / NS;  // chunks per window
+    constexpr int NBUF = x16_nbuf<SPLIT>();
+    constexpr int BUFCAP = x16_buf_cap<SPLIT>();
+    static_assert(NS == 1 || NS == 2, "n of 1 or 2");
+    // the staging buffers as distinct objects, so that the compiler can tell
+    // the copies into one from the reads of another
+    __shared__ __attribute__((aligned(256))) char xs0[BUFCAP];
+    __shared__ __attribute__((aligned(256))) char xs1[BUFCAP];
+    __shared__ __attribute__((aligned(256))) char xs2[NBUF == 3 ? BUFCAP : 16];
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int q = lane >> 4, p = lane & 15;
+    const int cs = m * ROWB + 32;   // chunk stride in LDS
+    const int rw = CPW * m;         // X rows per window
+    const int units = M / RU;
+
+    // this workgroup's tile: row block rb, 128 tokens from t0 (tiles of one
+    // token range are adjacent, so an XCD's workgroups share X in its L2)
+    const int tile = xcd_tile(blockIdx.x, gridDim.x);
+    const int rb = tile % row_blocks;
+    const int t0 = (tile / row_blocks) * kXTok;
+    const int row_w = rb * G::rows_wg + wave * G::rows_wave;  // first row of this wave
+    int ug[GW];                                               // this wave's units (clamped)
+#pragma unroll
+    for (int u = 0; u < GW; ++u) ug[u] = min((row_w + u * RU) / RU, units - 1);
+
+    // transposing reads: lane (q, p) reads, for read r, row o_r of the chunk
+    // of slot kb_slot(q, 4 r + p / 4), tokens 4 (p % 4) .. +3 of the sub-tile
+    uint32_t rbase[2];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+        int s = 0;
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq)
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk)
+                if (qq == q && kk == (p >> 2)) s = kb_slot(NS, qq, 4 * r + kk);
+        rbase[r] = (uint32_t)((s / NS) * cs + (p & 3) * 8);
+    }
+
+    // ---- staging
+    const float *Xf = reinterpret_cast<const float *>(X_);
+    const _Float16 *Xh = reinterpret_cast<const _Float16 *>(X_);
+    // SPLIT: item i of a window = (row i / 32, tokens 4 (i % 32) .. +3); lane
+    // takes items lane_g + k 64 NW (rows st_row0 + k SROWS, one token offset);
+    // items past the last are clamped to the last row (a duplicate writes the
+    // same bytes twice)
+    constexpr int SROWS = SPLIT ? 64 * NW / (kXTok / 4) : 1;
+    const int lane_g = wave * 64 + lane;
+    const int st_row0 = SPLIT ? lane_g / (kXTok / 4) : 0;
+    const int st_ti = lane_g % (kXTok / 4);
+    const uint32_t st_sub = (uint32_t)((st_ti >> 4) * 256 + (st_ti & 15) * 8);  // within a row
+    const int st_tok = min(t0 + 4 * st_ti, N - 4);   // tokens past N: never stored
+    // HALF: copy instruction j = wave + k NW moves 4 rows (16 lanes of 16
+    // bytes each): rows 4 j .. 4 j + 3 of the window, one chunk (m % 4 == 0),
+    // 1 KB contiguous in LDS; instructions past the last repeat the last one
+    // (same bytes to the same place), so every wave issues exactly NSTG copies
+    const int ninst = rw / 4;
+    const int cp_sub = lane >> 4;                 // row within the instruction's 4
+    const int cp_tok = 8 * (lane & 15);           // token offset within the tile
+    f4 stg[NSTG];
+    // item k of window w's staging
+    auto stage_one = [&](int w, char *buf, auto kc) __attribute__((always_inline)) {
+        constexpr int k = decltype(kc)::value;
+        const int k0 = w * rw;
+        if constexpr (SPLIT) {
+            const int row = min(st_row0 + k * SROWS, rw - 1);
+            const int xr = min(k0 + row, K - 1);           // rows past K: never selected
+            stg[k] = *reinterpret_cast<const f4 *>(Xf + (int64_t)xr * ldx + st_tok);
+        } else {
+            const int j = min(wave + k * NW, ninst - 1);   // uniform
+            const int row0 = 4 * j;                         // first row of the four, in the window
+            const int c = row0 / m, o = row0 - c * m;       // its chunk and offset (uniform)
+            const int xr = min(k0 + row0 + cp_sub, K - 1);
+            const int tok = min(t0 + cp_tok, N - 8);
+            lds_copy16(Xh + (int64_t)xr * ldx + tok, reinterpret_cast<_Float16 *>(buf + c * cs + o * ROWB));
+        }
+    };
+    auto stage_issue = [&](int w, char *buf) __attribute__((always_inline)) {
+        static_for<NSTG>([&](auto kc) { stage_one(w, buf, kc); });
+    };
+    // SPLIT: the registers of one window, split and written to LDS
+    auto stage_write = [&](char *buf) __attribute__((always_inline)) {
+        if constexpr (SPLIT) {
+            lds_char *lb = (lds_char *)buf;
+#pragma unroll
+            for (int k = 0; k < NSTG; ++k) {
+                const int row = min(st_row0 + k * SROWS, rw - 1);
+                const int c = row / m, o = row - c * m;
+                const uint32_t off = (uint32_t)(c * cs + o * ROWB) + st_sub;
+                _Float16 hi[4], lo[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    hi[i] = (_Float16)stg[k][i];
+                    // the remainder (exact in binary32) scaled by 2^11 (exact),
+                    // so that it stays a normal binary16 number down to |x| of
+                    // about 2^-14; the products with it are scaled back through
+                    // the weights (compute)
+                    lo[i] = (_Float16)((stg[k][i] - (float)hi[i]) * 2048.f);
+                }
+                *(lds_u2 *)(lb + off) = u32x2{pack_h2(hi[0], hi[1]), pack_h2(hi[2], hi[3])};
+                *(lds_u2 *)(lb + off + 128) = u32x2{pack_h2(lo[0], lo[1]), pack_h2(lo[2], lo[3])};
+            }
+        }
+    };
+
+    // ---- a window's prepared operands (windows past the last: the last one)
+    struct Ops {
+        h8 b[GW];
+        uint32_t o[GW];
+    };
+    // (binary16 8-row units: columns 8-15 are zero; those lanes load the
+    // fragment of column p - 8, so a unit's fragments are 512 distinct bytes,
+    // and zero it where it is used)
+    const int flane = (!SPLIT && !U16) ? (lane & ~8) : lane;
+    auto load_one = [&](int w, Ops &op, auto uc) __attribute__((always_inline)) {
+        constexpr int u = decltype(uc)::value;
+        const size_t e = ((size_t)ug[u] * nwin + min(w, nwin - 1)) * 64;
+        op.b[u] = frag[e + flane];
+        op.o[u] = offs[e + lane];
+    };
+    auto load_ops = [&](int w, Ops &op) __attribute__((always_inline)) {
+        static_for<GW>([&](auto uc) { load_one(w, op, uc); });
+    };
+    // A addresses of a window (byte offsets within its buffer)
+    auto addresses = [&](const Ops &op, uint32_t (&aa)[GW][2]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < GW; ++u) {
+            aa[u][0] = rbase[0] + (op.o[u] & 0xffu) * (uint32_t)ROWB;
+            aa[u][1] = rbase[1] + (op.o[u] >> 8) * (uint32_t)ROWB;
+        }
+    };
+
+    f4 acc[GW][kXTiles];
+#pragma unroll
+    for (int u = 0; u < GW; ++u)
+#pragma unroll
+        for (int t = 0; t < kXTiles; ++t) acc[u][t] = f4{0.f, 0.f, 0.f, 0.f};
+
+    // ---- the products of one window: NM instructions, each fed by two
+    // transposing reads issued PD instructions ahead
+    constexpr int NPL = SPLIT ? 2 : 1;
+    constexpr int NM = NPL * GW * kXTiles;
+    constexpr int PD = 3;
+    // The loads for later windows (NJ jobs) are issued between the
+    // instructions, one every JS of them, so that the load path works while
+    // the matrix cores do (issued all at once, they would queue on the load
+    // path while the matrix cores wait at the next barrier).
+    constexpr int NJ = NSTG + GW;
+    constexpr int JS = (SPLIT ? NM / 2 : NM) / NJ > 0 ? (SPLIT ? NM / 2 : NM) / NJ : 1;
+    auto compute = [&](const char *buf, const Ops &op, const uint32_t (&aa)[GW][2], auto &&job)
+        __attribute__((always_inline)) {
+        lds_char *lb = (lds_char *)buf;
+        h4 ra[PD][2];
+        auto issue = [&](auto ic) __attribute__((always_inline)) {
+            constexpr int i = decltype(ic)::value;
+            constexpr int pl = i / (GW * kXTiles), u = (i / kXTiles) % GW, t = i % kXTiles;
+            constexpr uint32_t toff = SPLIT ? (uint32_t)((t >> 2) * 256 + pl * 128 + (t & 3) * 32)
+                                            : (uint32_t)(t * 32);
+            ra[i % PD][0] = lds_read_tr(lb + aa[u][0] + toff);
+            ra[i % PD][1] = lds_read_tr(lb + aa[u][1] + toff);
+        };
+        // SPLIT: the lo plane of X holds remainders scaled by 2^11; its
+        // instructions take the weights scaled by 2^-11 (exact while normal)
+        h8 bl[GW];
+#pragma unroll
+        for (int u = 0; u < GW; ++u) {
+            if constexpr (SPLIT) {
+                const _Float16 k = (_Float16)(1.f / 2048.f);
+                bl[u] = op.b[u] * h8{k, k, k, k, k, k, k, k};
+            } else if constexpr (!U16) {
+                const h8 z = {};
+                bl[u] = p < 8 ? op.b[u] : z;
+            } else {
+                bl[u] = op.b[u];
+            }
+        }
+        static_for<PD>([&](auto ic) { issue(ic); });
+        static_for<NM>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            constexpr int pl = i / (GW * kXTiles), u = (i / kXTiles) % GW, t = i % kXTiles;
+            const h4 a0 = ra[i % PD][0], a1 = ra[i % PD][1];
+            const h8 a = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+            if constexpr (i + PD < NM) issue(std::integral_constant<int, i + PD>{});
+            acc[u][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, (SPLIT && pl == 0) ? op.b[u] : bl[u],
+                                                               acc[u][t], 0, 0, 0);
+            if constexpr (i % JS == 0 && i / JS < NJ) job(std::integral_constant<int, i / JS>{});
+        });
+        // jobs the instructions did not reach
+        static_for<NJ>([&](auto jc) {
+            constexpr int j = decltype(jc)::value;
+            if constexpr (j * JS >= NM) job(jc);
+        });
+    };
+
+    // ---- the pipeline.  HALF: operands and X copies two windows ahead
+    // (three buffers); at the end of window w the copies of w + 1 must have
+    // landed, and after them this wave issued only the operand loads of w + 2
+    // (2 GW) and the copies of w + 2 (NSTG): it waits until at most that many
+    // are outstanding.  SPLIT: operands and X one window ahead (X through
+    // registers, split and written after the products).
+    constexpr int DIST = SPLIT ? 1 : 2;     // windows ahead
+    constexpr int NOPS = DIST + 1;          // operand sets in rotation
+    char *const bufs[3] = {xs0, xs1, xs2};
+    Ops ops[NOPS];
+    uint32_t aa[2][GW][2];
+    load_ops(0, ops[0]);
+    if constexpr (DIST == 2) load_ops(1, ops[1]);
+    stage_issue(0, xs0);
+    if constexpr (!SPLIT) stage_issue(1, xs1);
+    stage_write(xs0);
+    wait_all_memory();
+    addresses(ops[0], aa[0]);
+    if constexpr (DIST == 2) addresses(ops[1], aa[1]);
+    __syncthreads();
+    // step w (W6 = w % 6, so that operand sets, address sets and buffers
+    // rotate statically): window w from bufs[W6 % NBUF]
+    auto step = [&](int w, auto w6c) __attribute__((always_inline)) {
+        constexpr int W6 = decltype(w6c)::value;
+        Ops &cur = ops[W6 % NOPS];
+        Ops &nxt = ops[(W6 + 1) % NOPS];
+        Ops &tgt = ops[(W6 + DIST) % NOPS];
+        uint32_t (&ac)[GW][2] = aa[W6 % 2];
+        uint32_t (&an)[GW][2] = aa[(W6 + 1) % 2];
+        // jobs: the copies (or X loads) of window w + DIST first, then its
+        // operands (so that at the window's end the copies of w + 1 are
+        // followed by exactly the window's own 2 GW + NSTG loads or more)
+        char *sbuf = bufs[(W6 + DIST) % NBUF];
+        const int ws = min(w + DIST, nwin - 1);
+        compute(bufs[W6 % NBUF], cur, ac, [&](auto jc) __attribute__((always_inline)) {
+            constexpr int j = decltype(jc)::value;
+            if constexpr (j < NSTG) stage_one(ws, sbuf, std::integral_constant<int, j>{});
+            else load_one(w + DIST, tgt, std::integral_constant<int, j - NSTG>{});
+        });
+        if constexpr (SPLIT) {
+            stage_write(bufs[(W6 + 1) % NBUF]);
+            addresses(nxt, an);
+            window_barrier<2 * GW>();  // operand loads of w + 1 may stay in flight
+        } else {
+            addresses(nxt, an);
+            window_barrier<2 * GW + NSTG>();
+        }
+    };
+    int w = 0;
+    for (; w + 6 <= nwin; w += 6) {
+        step(w + 0, std::integral_constant<int, 0>{});
+        step(w + 1, std::integral_constant<int, 1>{});
+        step(w + 2, std::integral_constant<int, 2>{});
+        step(w + 3, std::integral_constant<int, 3>{});
+        step(w + 4, std::integral_constant<int, 4>{});
+        step(w + 5, std::integral_constant<int, 5>{});
+    }
+    if (w < nwin) step(w, std::integral_constant<int, 0>{});
+    if (w + 1 < nwin) step(w + 1, std::integral_constant<int, 1>{});
+    if (w + 2 < nwin) step(w + 2, std::integral_constant<int, 2>{});
+    if (w + 3 < nwin) step(w + 3, std::integral_constant<int, 3>{});
+    if (w + 4 < nwin) step(w + 4, std::integral_constant<int, 4>{});
+
+    // ---- the outputs, through LDS: each wave writes its rows x 128 tokens
+    // into a region of its own (rows padded by 32 bytes, so that the 8 rows a
+    // write instruction touches fall on distinct banks), then stores whole
+    // rows, 16 bytes per lane (a full 256- or 512-byte run per row, instead of
+    // 32- or 64-byte pieces from the instruction's own layout)
+    constexpr int ES = SPLIT ? 4 : 2;
+    constexpr int RSTRIDE = kXTok * ES + 32;
+    constexpr int RB = G::rows_wave * RSTRIDE;       // one wave's region
+    constexpr int WPA = BUFCAP / RB;                 // regions per staging buffer
+    static_assert(WPA >= 1 && WPA * NBUF >= NW, "output regions fit the staging buffers");
+    window_barrier<0>();  // copies for windows past the last have landed; every wave is done
+    const int oreg = wave / WPA;
+    lds_char *ob = (lds_char *)(oreg == 0 ? xs0 : (NBUF == 2 || oreg == 1) ? xs1 : xs2) + (wave % WPA) * RB;
+#pragma unroll
+    for (int u = 0; u < GW; ++u) {
+        const float sc = SPLIT ? __builtin_ldexpf(1.f, -(int)scale[ug[u]]) : 1.f;
+#pragma unroll
+        for (int t = 0; t < kXTiles; ++t) {
+            f4 d = acc[u][t];
+            const uint32_t col = (uint32_t)((16 * t + 4 * q) * ES);
+            if constexpr (SPLIT) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) d[i] = add_row_ror8(d[i]) * sc;
+                if (p < 8) *(__attribute__((address_space(3))) f4 *)(ob + (u * RU + p) * RSTRIDE + col) = d;
+            } else {
+                if (U16 || p < 8)
+                    *(lds_u2 *)(ob + (u * RU + p) * RSTRIDE + col) =
+                        u32x2{pack_h2((_Float16)d[0], (_Float16)d[1]), pack_h2((_Float16)d[2], (_Float16)d[3])};
+            }
+        }
+    }
+    constexpr int LPR = kXTok * ES / 16;              // lanes per row
+    constexpr int RPI = 64 / LPR;                     // rows per instruction
+    const int orow = lane / LPR, ocol = lane % LPR;
+    const int tok = t0 + ocol * (16 / ES);
+#pragma unroll
+    for (int r0 = 0; r0 < G::rows_wave; r0 += RPI) {
+        const int r = r0 + orow;
+        const f4 v = *(__attribute__((address_space(3))) f4 *)(ob + r * RSTRIDE + ocol * 16);
+        const int row = row_w + r;
+        if (row < M && tok < N)
+            store_y(v, reinterpret_cast<f4 *>(reinterpret_cast<char *>(Y_) + ((int64_t)row * ldy + tok) * ES));
+    }
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- launchers
+
+namespace {
+
+// waves per workgroup (one workgroup per CU, 2 per SIMD)
+template <bool SPLIT> constexpr int x16_waves() { return 8; }
+
+// rows per unit of the prepared operands
+inline int x16_unit_rows(const nmg_layout *L) {
+    return L->dtype == NMG_F32 ? 8 : (L->g % 16 == 0 ? 16 : 8);
+}
+
+// staging items per lane (SPLIT) / copy instructions per wave (HALF) and window
+inline int x16_nstg(const nmg_layout *L) {
+    const bool split = L->dtype == NMG_F32;
+    const int rw = (kXSlots / L->n) * L->m;
+    if (split) {
+        const int lanes = 64 * x16_waves<true>();
+        return (rw * (kXTok / 4) + lanes - 1) / lanes;
+    }
+    const int inst = rw * (kXTok / 8) / 64;
+    return (inst + x16_waves<false>() - 1) / x16_waves<false>();
+}
+
+}  // namespace
+
+bool nmg_internal::x16_layout_supported(const nmg_layout *L) {
+    const bool split = L->dtype == NMG_F32;
+    const int64_t ldv = (int64_t)L->C * L->n;
+    if (L->n != 1 && L->n != 2) return false;
+    if (L->g % 8 != 0) return false;
+    if (!split && L->m % 4 != 0) return false;          // whole-wave LDS copies of 4 rows
+    const int rowb = split ? 512 : 256;
+    if (x16_buffer_bytes(L->n, L->m, rowb) > (split ? x16_buf_cap<true>() : x16_buf_cap<false>()))
+        return false;
+    if (x16_nstg(L) > 8) return false;
+    return (int64_t)L->M * ldv < ((int64_t)1 << 31);
+}
+
+int64_t nmg_internal::x16_prepared_bytes(const nmg_layout *L) {
+    if (!x16_layout_supported(L)) return -1;
+    return (int64_t)x16_prep_layout(L, x16_unit_rows(L)).bytes;
+}
+
+bool nmg_internal::x16_args_supported(const nmg_layout *L, const void *X, int64_t ldx,
+                                      const void *Y, int64_t ldy, int64_t N) {
+    const bool split = L->dtype == NMG_F32;
+    const size_t es = split ? 4 : 2;
+    // X rows on 16-byte boundaries; Y rows on 16 (binary32) / 8 (binary16)
+    const bool xa = X == nullptr || aligned(X, 16);
+    const bool ya = Y == nullptr || aligned(Y, split ? 16 : 8);
+    return x16_layout_supported(L) && xa && ya && ldx % (16 / es) == 0 && ldy % 4 == 0 &&
+           N % (split ? 4 : 8) == 0 && (int64_t)L->K * ldx < ((int64_t)1 << 31);
+}
+
+namespace {
+
+template <bool SPLIT, int NS, int RU>
+nmg_status launch_prepare_k(const nmg_layout *L, const void *values, const uint8_t *indices,
+                            void *prepared, hipStream_t stream) {
+    const XPrep P = x16_prep_layout(L, RU);
+    char *base = static_cast<char *>(prepared);
+    hipLaunchKernelGGL((k_x16_prepare<SPLIT, NS, RU>), dim3(P.units), dim3(64), 0, stream, values,
+                       indices, reinterpret_cast<h8 *>(base + P.frag),
+                       reinterpret_cast<uint16_t *>(base + P.offs),
+                       reinterpret_cast<int8_t *>(base + P.scale), L->M, L->m, L->g, L->C, P.nwin);
+    return launched();
+}
+
+template <bool SPLIT, int NS, bool U16, int GW, int NSTG>
+nmg_status launch_x16_k(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
+                        int N, void *Y, int64_t ldy, hipStream_t stream) {
+    constexpr int NW = x16_waves<SPLIT>();
+    using G = XGeom<SPLIT, U16, GW, NW>;
+    const XPrep P = x16_prep_layout(L, G::rows_unit);
+    const char *base = static_cast<const char *>(prepared);
+    const int row_blocks = (L->M + G::rows_wg - 1) / G::rows_wg;
+    const int grid = row_blocks * ((N + kXTok - 1) / kXTok);
+    hipLaunchKernelGGL((k_spmm_x16<SPLIT, NS, U16, GW, NW, NSTG>), dim3(grid), dim3(64 * NW), 0,
+                       stream, reinterpret_cast<const h8 *>(base + P.frag),
+                       reinterpret_cast<const uint16_t *>(base + P.offs),
+                       reinterpret_cast<const int8_t *>(base + P.scale), X, ldx, Y, ldy, L->M, L->K,
+                       N, L->m, P.nwin, row_blocks);
+    return launched();
+}
+
+template <bool SPLIT, int NS, bool U16, int GW>
+nmg_status launch_x16_s(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
+                        int N, void *Y, int64_t ldy, hipStream_t stream) {
+    switch (x16_nstg(L)) {
+        case 1: return launch_x16_k<SPLIT, NS, U16, GW, 1>(L, prepared, X, ldx, N, Y, ldy, stream);
+        case 2: return launch_x16_k<SPLIT, NS, U16, GW, 2>(L, prepared, X, ldx, N, Y, ldy, stream);
+        case 3: case 4: return launch_x16_k<SPLIT, NS, U16, GW, 4>(L, prepared, X, ldx, N, Y, ldy, stream);
+        case 5: case 6: return launch_x16_k<SPLIT, NS, U16, GW, 6>(L, prepared, X, ldx, N, Y, ldy, stream);
+        default: return launch_x16_k<SPLIT, NS, U16, GW, 8>(L, prepared, X, ldx, N, Y, ldy, stream);
+    }
+}
+
+// Units per wave.  More rows per workgroup share each staged X window (fewer
+// bytes through the CU's load path per instruction); fewer rows give more
+// workgroups.  Priced as rounds of workgroups (one per CU) times the rows of
+// one plus a fixed share for staging its X; binary32 at most 2 units (its
+// registers also hold the X being split), binary16 up to 3.
+template <bool SPLIT, bool U16>
+int x16_units(const nmg_layout *L, int64_t N) {
+    constexpr int ru = SPLIT ? 8 : (U16 ? 16 : 8);
+    const int cands[3] = {3, 2, 1};
+    const int64_t cus = device_cus();
+    const int64_t tt = (N + kXTok - 1) / kXTok;
+    int best = 1;
+    int64_t best_cost = -1;
+    for (int gw : cands) {
+        if (SPLIT && gw > 2) continue;
+        const int64_t rows = (int64_t)x16_waves<SPLIT>() * gw * ru;
+        const int64_t wgs = (L->M + rows - 1) / rows * tt;
+        const int64_t cost = (wgs + cus - 1) / cus * (rows + 64);
+        if (best_cost < 0 || cost < best_cost) {
+            best_cost = cost;
+            best = gw;
+        }
+    }
+    return best;
+}
+
+template <bool SPLIT, int NS, bool U16>
+nmg_status launch_x16_g(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
+                        int N, void *Y, int64_t ldy, hipStream_t stream) {
+    switch (x16_units<SPLIT, U16>(L, N)) {
+        case 3:
+            if constexpr (!SPLIT) return launch_x16_s<SPLIT, NS, U16, 3>(L, prepared, X, ldx, N, Y, ldy, stream);
+            return NMG_ERR_UNSUPPORTED;
+        case 2: return launch_x16_s<SPLIT, NS, U16, 2>(L, prepared, X, ldx, N, Y, ldy, stream);
+        default: return launch_x16_s<SPLIT, NS, U16, 1>(L, prepared, X, ldx, N, Y, ldy, stream);
+    }
+}
+
+}  // namespace
+
+nmg_status nmg_internal::x16_prepare(const nmg_layout *L, const void *values, const uint8_t *indices,
+                                     void *prepared, hipStream_t stream) {
+    const bool split = L->dtype == NMG_F32;
+    const int ru = x16_unit_rows(L);
+    if (split) return L->n == 1 ? launch_prepare_k<true, 1, 8>(L, values, indices, prepared, stream)
+                                : launch_prepare_k<true, 2, 8>(L, values, indices, prepared, stream);
+    if (ru == 16) return L->n == 1 ? launch_prepare_k<false, 1, 16>(L, values, indices, prepared, stream)
+                                   : launch_prepare_k<false, 2, 16>(L, values, indices, prepared, stream);
+    return L->n == 1 ? launch_prepare_k<false, 1, 8>(L, values, indices, prepared, stream)
+                     : launch_prepare_k<false, 2, 8>(L, values, indices, prepared, stream);
+}
+
+nmg_status nmg_internal::x16_product(const nmg_layout *L, const void *prepared, const void *X,
+                                     int64_t ldx, int N, void *Y, int64_t ldy, hipStream_t stream) {
+    if (L->dtype == NMG_F32)
+        return L->n == 1 ? launch_x16_g<true, 1, false>(L, prepared, X, ldx, N, Y, ldy, stream)
+                         : launch_x16_g<true, 2, false>(L, prepared, X, ldx, N, Y, ldy, stream);
+    const bool u16 = L->g % 16 == 0;
+    if (L->n == 1) return u16 ? launch_x16_g<false, 1, true>(L, prepared, X, ldx, N, Y, ldy, stream)
+                              : launch_x16_g<false, 1, false>(L, prepared, X, ldx, N, Y, ldy, stream);
+    return u16 ? launch_x16_g<false, 2, true>(L, prepared, X, ldx, N, Y, ldy, stream)
+               : launch_x16_g<false, 2, false>(L, prepared, X, ldx, N, Y, ldy, stream);
+}

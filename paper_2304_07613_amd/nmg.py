@@ -23,7 +23,7 @@ LIB_PATH = _build.LIB_PATH
 F32, F16 = 0, 1
 _DTYPE_CODE = {torch.float32: F32, torch.float16: F16}
 KERNELS = {"auto": 0, "valu": 1, "mfma": 2, "mfma_general": 3, "mfma_scalar": 4, "mfma_f16": 5,
-           "mfma_direct": 6, "smfmac_f16": 7, "valu_staged": 8}
+           "mfma_direct": 6, "smfmac_f16": 7, "valu_staged": 8, "mfma_wide": 9, "mfma_split": 10}
 _KERNEL_NAME = {v: k for k, v in KERNELS.items()}
 EPILOGUES = {"none": 0, "gelu": 1, "add": 2}
 
@@ -90,6 +90,9 @@ def lib():
         "nmg_p_spmm_with": ([pp, ctypes.c_int, vp, vp, vp, i64, i64, vp, i64, vp], ctypes.c_int),
         "nmg_p_refine": ([pp, vp, i64, vp, vp, vp], ctypes.c_int),
         "nmg_p_densify": ([pp, vp, vp, vp, i64, vp], ctypes.c_int),
+        "nmg_x16_prepared_bytes": ([lp], i64),
+        "nmg_x16_prepare": ([lp, vp, vp, vp, vp], ctypes.c_int),
+        "nmg_spmm_x16": ([lp, vp, vp, i64, i64, vp, i64, vp], ctypes.c_int),
         "nmg_status_str": ([ctypes.c_int], ctypes.c_char_p),
         "nmg_version": ([], ctypes.c_char_p),
     }
@@ -214,9 +217,43 @@ def repack(W: torch.Tensor, indices: torch.Tensor, layout: Layout) -> torch.Tens
     return values
 
 
+# kernel families that run on prepared operands (nmg_x16_prepare +
+# nmg_spmm_x16), and the element type each takes
+X16_KERNELS = {"mfma_wide": torch.float16, "mfma_split": torch.float32}
+
+
+def x16_prepare(values, indices, layout: Layout) -> torch.Tensor:
+    """``nmg_x16_prepare``: the prepared operands of a packed weight (bytes)."""
+    _need_cuda(values, indices)
+    nbytes = lib().nmg_x16_prepared_bytes(ctypes.byref(layout.c))
+    if nbytes < 0:
+        raise NmgError(ERR_UNSUPPORTED, "nmg_x16_prepared_bytes")
+    prepared = torch.empty(int(nbytes), dtype=torch.uint8, device=values.device)
+    _check(lib().nmg_x16_prepare(ctypes.byref(layout.c), _ptr(values), _ptr(indices),
+                                 _ptr(prepared), _stream(values)), "nmg_x16_prepare")
+    return prepared
+
+
+def spmm_x16_into(layout: Layout, prepared, X, Y):
+    """``nmg_spmm_x16`` into a caller-allocated Y (M x N)."""
+    _need_cuda(prepared, X, Y)
+    if X.dtype != layout.dtype or Y.dtype != layout.dtype:
+        raise TypeError("dtype mismatch")
+    if X.shape[0] != layout.K or Y.shape[0] != layout.M or Y.shape[1] != X.shape[1]:
+        raise ValueError("X must be K x N and Y M x N")
+    _check(lib().nmg_spmm_x16(ctypes.byref(layout.c), _ptr(prepared), _ptr(X), _rows(X, "X"),
+                              X.shape[1], _ptr(Y), _rows(Y, "Y"), _stream(X)), "nmg_spmm_x16")
+
+
 def spmm_into(layout: Layout, values, indices, X, Y, kernel: str = "auto"):
-    """``nmg_spmm_with`` into a caller-allocated Y (M x N)."""
+    """``nmg_spmm_with`` into a caller-allocated Y (M x N); the families of
+    X16_KERNELS go through ``nmg_x16_prepare`` + ``nmg_spmm_x16``."""
     _need_cuda(values, indices, X, Y)
+    if kernel in X16_KERNELS:
+        if X16_KERNELS[kernel] != layout.dtype:
+            raise NmgError(ERR_UNSUPPORTED, f"{kernel} takes {X16_KERNELS[kernel]}")
+        spmm_x16_into(layout, x16_prepare(values, indices, layout), X, Y)
+        return
     if X.dtype != layout.dtype or Y.dtype != layout.dtype or values.dtype != layout.dtype:
         raise TypeError("dtype mismatch")
     if X.shape[0] != layout.K or Y.shape[0] != layout.M or Y.shape[1] != X.shape[1]:
@@ -256,6 +293,17 @@ def spmm_epilogue(values, indices, X, layout: Layout, epilogue: str = "none", R=
     _need_cuda(Y)
     if Y.dtype != layout.dtype or tuple(Y.shape) != (layout.M, N):
         raise ValueError("Y must be M x N of the layout's dtype")
+    if kernel in X16_KERNELS:
+        # the product, then the elementwise pass (no fused epilogue here)
+        P = spmm(values, indices, X, layout, kernel)
+        if epilogue == "gelu":
+            P = gelu(P)
+        elif epilogue == "add":
+            if R is None:
+                raise ValueError("the add epilogue needs R")
+            P = add(P, R.contiguous())
+        Y.copy_(P)
+        return Y
     rp, ldr = ctypes.c_void_p(0), 0
     if epilogue == "add":
         if R is None:
