@@ -65,6 +65,8 @@ def parse():
     ap.add_argument("--workload", type=int, choices=(1, 2, 3), default=2)
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--stack", action="store_true")
+    ap.add_argument("--stack-kernels", default=None,
+                    help="with --stack: name=family items, comma-separated (qkv, ao, up, down)")
     ap.add_argument("--stack-layer", type=int, choices=(0, 1, 2, 3), default=None,
                     help="one projection of the fp16 stack (QKV, attention-out, FFN up, FFN down) "
                          "timed like --workload, with the other kernel families")
@@ -418,8 +420,15 @@ def stack(ctx, args):
     """Forward of the 12-layer fp16 linear stack (48 sparse products, 12 GELU,
     24 residual sums), weights compressed once beforehand."""
     torch, nmg, synth = ctx.torch, ctx.nmg, ctx.synth
+    from paper_2304_07613_amd import stack as stack_mod
     from paper_2304_07613_amd.stack import LinearStack
-    st = LinearStack.from_workload(4, nmg, keep_dense=False)
+    kernels = dict(stack_mod.DEFAULT_KERNELS)
+    for item in filter(None, (args.stack_kernels or "").split(",")):
+        name, _, fam = item.partition("=")
+        if name not in kernels or fam not in nmg.KERNELS:
+            raise SystemExit(f"--stack-kernels: bad item {item!r}")
+        kernels[name] = fam
+    st = LinearStack.from_workload(4, nmg, keep_dense=False, kernels=kernels)
     torch.cuda.synchronize()
     x = synth.normal((synth.BERT_HIDDEN, synth.BERT_TOKENS), synth.seed_for(4, 0, "X"), 1.0,
                      torch.float16).to(ctx.dev)
@@ -440,6 +449,7 @@ def stack(ctx, args):
                       "ms_per_forward": round(ms, 4),
                       "tokens_per_s": round(synth.BERT_TOKENS / (ms * 1e-3), 1),
                       "dtype": "f16 (binary32 accumulate)", "layers": 12, "reps": reps,
+                      "kernels": kernels,
                       "finite": bool(torch.isfinite(y.float()).all())}), flush=True)
 
 

@@ -225,18 +225,21 @@ nmg_kernel nmg_spmm_auto_kernel(const nmg_layout *layout, int64_t N);
  * Layouts taken: n in {1, 2}; g % 8 == 0; the staging of one window (32
  * k-slots = 32 / n chunks of m X rows, 128 tokens per row) within the LDS
  * buffers: binary16 needs m % 4 == 0 and (32 / n) (256 m + 32) <= 53248
- * (m = 4 or 8 at n = 1, m <= 12 at n = 2); binary32 needs (32 / n) (512 m +
- * 32) <= 81920 (m <= 4 at n = 1, m <= 9 at n = 2); M * C * n < 2^31.
+ * (m = 4 at n = 1; m = 4, 8 or 12 at n = 2); binary32 needs (32 / n) (512 m +
+ * 32) <= 81920 and m <= 8 (m <= 4 at n = 1, m <= 8 at n = 2); M * C * n <
+ * 2^31.
  *
  * Binary32 (MFMA_SPLIT) is not binary32 arithmetic: every weight w (scaled by
  * a power of two per 8 rows that puts the largest |w| of those rows into
- * [2^13, 2^14)) and every X entry x is carried as hi = fp16(v), lo = fp16(v -
- * hi), and all four products of the parts are summed in binary32; the
- * output is scaled back exactly.  Per output, |Y - W_s X| is at most about
- * 2^-20 B + 2^-25 sum_k |w_k| + (binary32 summation error), B = sum_k |w_k
- * x_k| over the kept k, for finite X with |x| < 65504 -- within the 1e-5 B
- * of the binary32 families whenever the kept X entries are not many orders
- * of magnitude below 2^-5 on average.  NMG_KERNEL_AUTO never chooses it.
+ * [2^13, 2^14)) is carried as hi = fp16(w), lo = fp16(w - hi), every X entry
+ * x as hi = fp16(x), lo = fp16((x - hi) 2^11), and all four products of the
+ * parts are summed in binary32 (the products with x's lo part against weight
+ * parts scaled by 2^-11); the output is scaled back exactly.  Per output,
+ * |Y - W_s X| is at most about 2^-21 B + 2^-36 sum_k |w_k| + 2^-37 w_max
+ * sum_k |x_k| + (binary32 summation error), B = sum_k |w_k x_k| over the
+ * kept k and w_max the largest |w| of the output's 8-row block, for finite X
+ * with |x| < 65504 -- within the 1e-5 B of the binary32 families unless
+ * nearly all of B comes from a few k.  NMG_KERNEL_AUTO never chooses it.
  */
 
 /* Bytes of the prepared operands of a layout; -1 for an invalid layout or one
@@ -258,6 +261,17 @@ nmg_status nmg_x16_prepare(const nmg_layout *layout, const void *values, const u
  * NMG_ERR_UNSUPPORTED. */
 nmg_status nmg_spmm_x16(const nmg_layout *layout, const void *prepared, const void *X,
                         int64_t ldx, int64_t N, void *Y, int64_t ldy, hipStream_t stream);
+
+/* nmg_spmm_x16 with an epilogue applied as the outputs are stored:
+ * NMG_EPILOGUE_NONE (= nmg_spmm_x16) or NMG_EPILOGUE_ADD, Y = P + R computed
+ * as nmg_add computes it (P the product rounded to the element type); R is
+ * M x N, leading dimension ldr >= N, 16-byte aligned with ldr a multiple of
+ * 16 bytes (else NMG_ERR_UNSUPPORTED), and must not overlap Y
+ * (NMG_ERR_PARAM).  NMG_EPILOGUE_GELU: NMG_ERR_UNSUPPORTED. */
+nmg_status nmg_spmm_x16_epilogue(const nmg_layout *layout, const void *prepared,
+                                 nmg_epilogue epilogue, const void *X, int64_t ldx, int64_t N,
+                                 const void *R, int64_t ldr, void *Y, int64_t ldy,
+                                 hipStream_t stream);
 
 /* n:m:g -> dense (end of Section 5.2): W_out (M x K, leading dimension
  * ldw >= K) gets the kept weights at their columns and +0 elsewhere. */

@@ -236,6 +236,9 @@ nmg_status nmg_spmm_epilogue(const nmg_layout *L, nmg_kernel kernel, nmg_epilogu
             if (!spmm_valu_staged_supported(L, X, ldx, N)) return NMG_ERR_UNSUPPORTED;
             st = spmm_valu_staged(a);
             break;
+        case NMG_KERNEL_MFMA_WIDE:
+        case NMG_KERNEL_MFMA_SPLIT:
+            return NMG_ERR_UNSUPPORTED;  // these run on prepared operands only
         default:
             return NMG_ERR_PARAM;
     }
@@ -355,16 +358,38 @@ nmg_status nmg_x16_prepare(const nmg_layout *L, const void *values, const uint8_
     return x16_prepare(L, values, indices, prepared, stream);
 }
 
-nmg_status nmg_spmm_x16(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
-                        int64_t N, void *Y, int64_t ldy, hipStream_t stream) {
+nmg_status nmg_spmm_x16_epilogue(const nmg_layout *L, const void *prepared, nmg_epilogue epi,
+                                 const void *X, int64_t ldx, int64_t N, const void *R, int64_t ldr,
+                                 void *Y, int64_t ldy, hipStream_t stream) {
     nmg_status st = check_layout(L);
     if (st != NMG_OK) return st;
     if (!prepared || !X || !Y) return NMG_ERR_NULL;
     if (N < 1 || N > INT32_MAX || ldx < N || ldy < N) return NMG_ERR_PARAM;
+    if (epi != NMG_EPILOGUE_NONE && epi != NMG_EPILOGUE_GELU && epi != NMG_EPILOGUE_ADD)
+        return NMG_ERR_PARAM;
+    if (epi == NMG_EPILOGUE_GELU) return NMG_ERR_UNSUPPORTED;
     if (!aligned(prepared, 16)) return NMG_ERR_ALIGN;
     if (!x16_args_supported(L, X, ldx, Y, ldy, N)) return NMG_ERR_UNSUPPORTED;
+    if (epi == NMG_EPILOGUE_ADD) {
+        if (!R) return NMG_ERR_NULL;
+        if (ldr < N) return NMG_ERR_PARAM;
+        // R is read 16 bytes at a time, on Y's pattern
+        if (!aligned(R, 16) || ldr % (16 / (int64_t)elem_size(L->dtype)) != 0)
+            return NMG_ERR_UNSUPPORTED;
+        const size_t es = elem_size(L->dtype);
+        const uintptr_t r0 = reinterpret_cast<uintptr_t>(R), y0 = reinterpret_cast<uintptr_t>(Y);
+        const uintptr_t r1 = r0 + (uintptr_t)(((int64_t)(L->M - 1) * ldr + N) * (int64_t)es);
+        const uintptr_t y1 = y0 + (uintptr_t)(((int64_t)(L->M - 1) * ldy + N) * (int64_t)es);
+        if (r0 < y1 && y0 < r1) return NMG_ERR_PARAM;
+    }
     prelaunch();
-    return x16_product(L, prepared, X, ldx, (int)N, Y, ldy, stream);
+    return x16_product(L, prepared, X, ldx, (int)N, Y, ldy, (int)epi, R, ldr, stream);
+}
+
+nmg_status nmg_spmm_x16(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
+                        int64_t N, void *Y, int64_t ldy, hipStream_t stream) {
+    return nmg_spmm_x16_epilogue(L, prepared, NMG_EPILOGUE_NONE, X, ldx, N, nullptr, 0, Y, ldy,
+                                 stream);
 }
 
 nmg_status nmg_densify(const nmg_layout *L, const void *values, const uint8_t *indices,

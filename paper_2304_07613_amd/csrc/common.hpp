@@ -125,7 +125,8 @@ int64_t x16_prepared_bytes(const nmg_layout *L);
 nmg_status x16_prepare(const nmg_layout *L, const void *values, const uint8_t *indices,
                        void *prepared, hipStream_t stream);
 nmg_status x16_product(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
-                       int N, void *Y, int64_t ldy, hipStream_t stream);
+                       int N, void *Y, int64_t ldy, int epi, const void *R, int64_t ldr,
+                       hipStream_t stream);
 
 nmg_status check_p_layout(const nmg_p_layout *L);
 int p_pattern_count(int m, int n);

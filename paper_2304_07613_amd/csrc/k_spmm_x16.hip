@@ -255,11 +255,13 @@ __global__ __launch_bounds__(64) void k_x16_prepare(const void *__restrict__ val
 
 // ---------------------------------------------------------------- the product
 
+// R_ == nullptr: Y = P; else Y = P + R (the sum in binary32 of the product
+// rounded to the element type and R, rounded again)
 template <bool SPLIT, int NS, bool U16, int GW, int NW, int NSTG>
 __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
     const h8 *__restrict__ frag, const uint16_t *__restrict__ offs, const int8_t *__restrict__ scale,
-    const void *__restrict__ X_, int64_t ldx, void *__restrict__ Y_, int64_t ldy, int M, int K,
-    int N, int m, int nwin, int row_blocks) {
+    const void *__restrict__ X_, int64_t ldx, void *__restrict__ Y_, int64_t ldy,
+    const void *__restrict__ R_, int64_t ldr, int M, int K, int N, int m, int nwin, int row_blocks) {
     using G = XGeom<SPLIT, U16, GW, NW>;
     constexpr int RU = G::rows_unit, ROWB = G::row_bytes;
     constexpr int CPW = kXSlots / NS;  // chunks per window
@@ -321,6 +323,9 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
     // 1 KB contiguous in LDS; instructions past the last repeat the last one
     // (same bytes to the same place), so every wave issues exactly NSTG copies
     const int ninst = rw / 4;
+    // r / m for the rows of a window (r < 32 m, m <= 45) by a multiply
+    const uint32_t inv_m = (65536u + (uint32_t)m - 1) / (uint32_t)m;
+    auto div_m = [&](int r) __attribute__((always_inline)) { return (int)(((uint32_t)r * inv_m) >> 16); };
     const int cp_sub = lane >> 4;                 // row within the instruction's 4
     const int cp_tok = 8 * (lane & 15);           // token offset within the tile
     f4 stg[NSTG];
@@ -335,7 +340,7 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
         } else {
             const int j = min(wave + k * NW, ninst - 1);   // uniform
             const int row0 = 4 * j;                         // first row of the four, in the window
-            const int c = row0 / m, o = row0 - c * m;       // its chunk and offset (uniform)
+            const int c = div_m(row0), o = row0 - c * m;    // its chunk and offset (uniform)
             const int xr = min(k0 + row0 + cp_sub, K - 1);
             const int tok = min(t0 + cp_tok, N - 8);
             lds_copy16(Xh + (int64_t)xr * ldx + tok, reinterpret_cast<_Float16 *>(buf + c * cs + o * ROWB));
@@ -345,28 +350,29 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
         static_for<NSTG>([&](auto kc) { stage_one(w, buf, kc); });
     };
     // SPLIT: the registers of one window, split and written to LDS
-    auto stage_write = [&](char *buf) __attribute__((always_inline)) {
+    auto stage_write_one = [&](char *buf, auto kc) __attribute__((always_inline)) {
+        constexpr int k = decltype(kc)::value;
         if constexpr (SPLIT) {
             lds_char *lb = (lds_char *)buf;
+            const int row = min(st_row0 + k * SROWS, rw - 1);
+            const int c = div_m(row), o = row - c * m;
+            const uint32_t off = (uint32_t)(c * cs + o * ROWB) + st_sub;
+            _Float16 hi[4], lo[4];
 #pragma unroll
-            for (int k = 0; k < NSTG; ++k) {
-                const int row = min(st_row0 + k * SROWS, rw - 1);
-                const int c = row / m, o = row - c * m;
-                const uint32_t off = (uint32_t)(c * cs + o * ROWB) + st_sub;
-                _Float16 hi[4], lo[4];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    hi[i] = (_Float16)stg[k][i];
-                    // the remainder (exact in binary32) scaled by 2^11 (exact),
-                    // so that it stays a normal binary16 number down to |x| of
-                    // about 2^-14; the products with it are scaled back through
-                    // the weights (compute)
-                    lo[i] = (_Float16)((stg[k][i] - (float)hi[i]) * 2048.f);
-                }
-                *(lds_u2 *)(lb + off) = u32x2{pack_h2(hi[0], hi[1]), pack_h2(hi[2], hi[3])};
-                *(lds_u2 *)(lb + off + 128) = u32x2{pack_h2(lo[0], lo[1]), pack_h2(lo[2], lo[3])};
+            for (int i = 0; i < 4; ++i) {
+                hi[i] = (_Float16)stg[k][i];
+                // the remainder (exact in binary32) scaled by 2^11 (exact), so
+                // that it stays a normal binary16 number down to |x| of about
+                // 2^-14; the products with it are scaled back through the
+                // weights (compute)
+                lo[i] = (_Float16)((stg[k][i] - (float)hi[i]) * 2048.f);
             }
+            *(lds_u2 *)(lb + off) = u32x2{pack_h2(hi[0], hi[1]), pack_h2(hi[2], hi[3])};
+            *(lds_u2 *)(lb + off + 128) = u32x2{pack_h2(lo[0], lo[1]), pack_h2(lo[2], lo[3])};
         }
+    };
+    auto stage_write = [&](char *buf) __attribute__((always_inline)) {
+        static_for<NSTG>([&](auto kc) { stage_write_one(buf, kc); });
     };
 
     // ---- a window's prepared operands (windows past the last: the last one)
@@ -413,8 +419,12 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
     // path while the matrix cores wait at the next barrier).
     constexpr int NJ = NSTG + GW;
     constexpr int JS = (SPLIT ? NM / 2 : NM) / NJ > 0 ? (SPLIT ? NM / 2 : NM) / NJ : 1;
-    auto compute = [&](const char *buf, const Ops &op, const uint32_t (&aa)[GW][2], auto &&job)
-        __attribute__((always_inline)) {
+    // SPLIT: the X of window w + 1, loaded by the jobs, is split and written
+    // to LDS (NSTG items) between the instructions of the second half, one
+    // every WS of them.
+    constexpr int WS = (NM / 2) / NSTG > 0 ? (NM / 2) / NSTG : 1;
+    auto compute = [&](const char *buf, const Ops &op, const uint32_t (&aa)[GW][2], auto &&job,
+                       auto &&post) __attribute__((always_inline)) {
         lds_char *lb = (lds_char *)buf;
         h4 ra[PD][2];
         auto issue = [&](auto ic) __attribute__((always_inline)) {
@@ -450,11 +460,17 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
             acc[u][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, (SPLIT && pl == 0) ? op.b[u] : bl[u],
                                                                acc[u][t], 0, 0, 0);
             if constexpr (i % JS == 0 && i / JS < NJ) job(std::integral_constant<int, i / JS>{});
+            if constexpr (i >= NM / 2 && (i - NM / 2) % WS == 0 && (i - NM / 2) / WS < NSTG)
+                post(std::integral_constant<int, (i - NM / 2) / WS>{});
         });
-        // jobs the instructions did not reach
+        // jobs and post jobs the instructions did not reach
         static_for<NJ>([&](auto jc) {
             constexpr int j = decltype(jc)::value;
             if constexpr (j * JS >= NM) job(jc);
+        });
+        static_for<NSTG>([&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            if constexpr (NM / 2 + k * WS >= NM) post(kc);
         });
     };
 
@@ -492,13 +508,15 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
         // followed by exactly the window's own 2 GW + NSTG loads or more)
         char *sbuf = bufs[(W6 + DIST) % NBUF];
         const int ws = min(w + DIST, nwin - 1);
-        compute(bufs[W6 % NBUF], cur, ac, [&](auto jc) __attribute__((always_inline)) {
-            constexpr int j = decltype(jc)::value;
-            if constexpr (j < NSTG) stage_one(ws, sbuf, std::integral_constant<int, j>{});
-            else load_one(w + DIST, tgt, std::integral_constant<int, j - NSTG>{});
-        });
+        compute(
+            bufs[W6 % NBUF], cur, ac,
+            [&](auto jc) __attribute__((always_inline)) {
+                constexpr int j = decltype(jc)::value;
+                if constexpr (j < NSTG) stage_one(ws, sbuf, std::integral_constant<int, j>{});
+                else load_one(w + DIST, tgt, std::integral_constant<int, j - NSTG>{});
+            },
+            [&](auto kc) __attribute__((always_inline)) { stage_write_one(sbuf, kc); });
         if constexpr (SPLIT) {
-            stage_write(bufs[(W6 + 1) % NBUF]);
             addresses(nxt, an);
             window_barrier<2 * GW>();  // operand loads of w + 1 may stay in flight
         } else {
@@ -559,10 +577,24 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
 #pragma unroll
     for (int r0 = 0; r0 < G::rows_wave; r0 += RPI) {
         const int r = r0 + orow;
-        const f4 v = *(__attribute__((address_space(3))) f4 *)(ob + r * RSTRIDE + ocol * 16);
+        f4 v = *(__attribute__((address_space(3))) f4 *)(ob + r * RSTRIDE + ocol * 16);
         const int row = row_w + r;
-        if (row < M && tok < N)
+        if (row < M && tok < N) {
+            if (R_ != nullptr) {
+                const f4 rv = *reinterpret_cast<const f4 *>(reinterpret_cast<const char *>(R_) +
+                                                            ((int64_t)row * ldr + tok) * ES);
+                if constexpr (SPLIT) {
+                    v = v + rv;
+                } else {
+                    const h8 a = __builtin_bit_cast(h8, v), b = __builtin_bit_cast(h8, rv);
+                    h8 o;
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) o[i] = (_Float16)((float)a[i] + (float)b[i]);
+                    v = __builtin_bit_cast(f4, o);
+                }
+            }
             store_y(v, reinterpret_cast<f4 *>(reinterpret_cast<char *>(Y_) + ((int64_t)row * ldy + tok) * ES));
+        }
     }
 }
 
@@ -637,33 +669,62 @@ nmg_status launch_prepare_k(const nmg_layout *L, const void *values, const uint8
     return launched();
 }
 
+struct X16Out {
+    void *Y;
+    int64_t ldy;
+    int epi;
+    const void *R;
+    int64_t ldr;
+};
+
 template <bool SPLIT, int NS, bool U16, int GW, int NSTG>
 nmg_status launch_x16_k(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
-                        int N, void *Y, int64_t ldy, hipStream_t stream) {
+                        int N, const X16Out &o, hipStream_t stream) {
     constexpr int NW = x16_waves<SPLIT>();
     using G = XGeom<SPLIT, U16, GW, NW>;
     const XPrep P = x16_prep_layout(L, G::rows_unit);
     const char *base = static_cast<const char *>(prepared);
     const int row_blocks = (L->M + G::rows_wg - 1) / G::rows_wg;
     const int grid = row_blocks * ((N + kXTok - 1) / kXTok);
+    const h8 *fr = reinterpret_cast<const h8 *>(base + P.frag);
+    const uint16_t *of = reinterpret_cast<const uint16_t *>(base + P.offs);
+    const int8_t *sc = reinterpret_cast<const int8_t *>(base + P.scale);
     hipLaunchKernelGGL((k_spmm_x16<SPLIT, NS, U16, GW, NW, NSTG>), dim3(grid), dim3(64 * NW), 0,
-                       stream, reinterpret_cast<const h8 *>(base + P.frag),
-                       reinterpret_cast<const uint16_t *>(base + P.offs),
-                       reinterpret_cast<const int8_t *>(base + P.scale), X, ldx, Y, ldy, L->M, L->K,
-                       N, L->m, P.nwin, row_blocks);
+                       stream, fr, of, sc, X, ldx, o.Y, o.ldy,
+                       o.epi == NMG_EPILOGUE_ADD ? o.R : nullptr, o.ldr, L->M, L->K, N, L->m,
+                       P.nwin, row_blocks);
     return launched();
+}
+
+// The staging job counts the supported layouts have (x16_nstg, rounded up to
+// the instantiated 2, 4, 6, 8): binary16 windows of 32 m / n rows take m / n
+// jobs (m = 4 at n = 1; 4, 8, 12 at n = 2), binary32 ones 2 m / n (m = 1..4 at
+// n = 1, 2..8 at n = 2)
+template <bool SPLIT, int NS>
+constexpr bool x16_nstg_used(int s) {
+    if constexpr (SPLIT) return s >= 2;
+    return NS == 1 ? s == 4 : (s >= 2 && s <= 6);
 }
 
 template <bool SPLIT, int NS, bool U16, int GW>
 nmg_status launch_x16_s(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
-                        int N, void *Y, int64_t ldy, hipStream_t stream) {
-    switch (x16_nstg(L)) {
-        case 1: return launch_x16_k<SPLIT, NS, U16, GW, 1>(L, prepared, X, ldx, N, Y, ldy, stream);
-        case 2: return launch_x16_k<SPLIT, NS, U16, GW, 2>(L, prepared, X, ldx, N, Y, ldy, stream);
-        case 3: case 4: return launch_x16_k<SPLIT, NS, U16, GW, 4>(L, prepared, X, ldx, N, Y, ldy, stream);
-        case 5: case 6: return launch_x16_k<SPLIT, NS, U16, GW, 6>(L, prepared, X, ldx, N, Y, ldy, stream);
-        default: return launch_x16_k<SPLIT, NS, U16, GW, 8>(L, prepared, X, ldx, N, Y, ldy, stream);
+                        int N, const X16Out &Y, hipStream_t stream) {
+    const int s = x16_nstg(L);
+    const int r = s <= 2 ? 2 : s <= 4 ? 4 : s <= 6 ? 6 : 8;
+#define X16_CASE(V)                                                                        \
+    case V:                                                                                \
+        if constexpr (x16_nstg_used<SPLIT, NS>(V))                                         \
+            return launch_x16_k<SPLIT, NS, U16, GW, V>(L, prepared, X, ldx, N, Y, stream); \
+        break;
+    switch (r) {
+        X16_CASE(2)
+        X16_CASE(4)
+        X16_CASE(6)
+        X16_CASE(8)
+        default: break;
     }
+#undef X16_CASE
+    return NMG_ERR_UNSUPPORTED;
 }
 
 // Units per wave.  More rows per workgroup share each staged X window (fewer
@@ -694,13 +755,13 @@ int x16_units(const nmg_layout *L, int64_t N) {
 
 template <bool SPLIT, int NS, bool U16>
 nmg_status launch_x16_g(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
-                        int N, void *Y, int64_t ldy, hipStream_t stream) {
+                        int N, const X16Out &Y, hipStream_t stream) {
     switch (x16_units<SPLIT, U16>(L, N)) {
         case 3:
-            if constexpr (!SPLIT) return launch_x16_s<SPLIT, NS, U16, 3>(L, prepared, X, ldx, N, Y, ldy, stream);
+            if constexpr (!SPLIT) return launch_x16_s<SPLIT, NS, U16, 3>(L, prepared, X, ldx, N, Y, stream);
             return NMG_ERR_UNSUPPORTED;
-        case 2: return launch_x16_s<SPLIT, NS, U16, 2>(L, prepared, X, ldx, N, Y, ldy, stream);
-        default: return launch_x16_s<SPLIT, NS, U16, 1>(L, prepared, X, ldx, N, Y, ldy, stream);
+        case 2: return launch_x16_s<SPLIT, NS, U16, 2>(L, prepared, X, ldx, N, Y, stream);
+        default: return launch_x16_s<SPLIT, NS, U16, 1>(L, prepared, X, ldx, N, Y, stream);
     }
 }
 
@@ -719,13 +780,15 @@ nmg_status nmg_internal::x16_prepare(const nmg_layout *L, const void *values, co
 }
 
 nmg_status nmg_internal::x16_product(const nmg_layout *L, const void *prepared, const void *X,
-                                     int64_t ldx, int N, void *Y, int64_t ldy, hipStream_t stream) {
+                                     int64_t ldx, int N, void *Yp, int64_t ldy, int epi,
+                                     const void *R, int64_t ldr, hipStream_t stream) {
+    const X16Out Y{Yp, ldy, epi, R, ldr};
     if (L->dtype == NMG_F32)
-        return L->n == 1 ? launch_x16_g<true, 1, false>(L, prepared, X, ldx, N, Y, ldy, stream)
-                         : launch_x16_g<true, 2, false>(L, prepared, X, ldx, N, Y, ldy, stream);
+        return L->n == 1 ? launch_x16_g<true, 1, false>(L, prepared, X, ldx, N, Y, stream)
+                         : launch_x16_g<true, 2, false>(L, prepared, X, ldx, N, Y, stream);
     const bool u16 = L->g % 16 == 0;
-    if (L->n == 1) return u16 ? launch_x16_g<false, 1, true>(L, prepared, X, ldx, N, Y, ldy, stream)
-                              : launch_x16_g<false, 1, false>(L, prepared, X, ldx, N, Y, ldy, stream);
-    return u16 ? launch_x16_g<false, 2, true>(L, prepared, X, ldx, N, Y, ldy, stream)
-               : launch_x16_g<false, 2, false>(L, prepared, X, ldx, N, Y, ldy, stream);
+    if (L->n == 1) return u16 ? launch_x16_g<false, 1, true>(L, prepared, X, ldx, N, Y, stream)
+                              : launch_x16_g<false, 1, false>(L, prepared, X, ldx, N, Y, stream);
+    return u16 ? launch_x16_g<false, 2, true>(L, prepared, X, ldx, N, Y, stream)
+               : launch_x16_g<false, 2, false>(L, prepared, X, ldx, N, Y, stream);
 }

@@ -93,6 +93,8 @@ def lib():
         "nmg_x16_prepared_bytes": ([lp], i64),
         "nmg_x16_prepare": ([lp, vp, vp, vp, vp], ctypes.c_int),
         "nmg_spmm_x16": ([lp, vp, vp, i64, i64, vp, i64, vp], ctypes.c_int),
+        "nmg_spmm_x16_epilogue": ([lp, vp, ctypes.c_int, vp, i64, i64, vp, i64, vp, i64, vp],
+                                  ctypes.c_int),
         "nmg_status_str": ([ctypes.c_int], ctypes.c_char_p),
         "nmg_version": ([], ctypes.c_char_p),
     }
@@ -245,6 +247,33 @@ def spmm_x16_into(layout: Layout, prepared, X, Y):
                               X.shape[1], _ptr(Y), _rows(Y, "Y"), _stream(X)), "nmg_spmm_x16")
 
 
+def spmm_x16_epilogue(layout: Layout, prepared, X, epilogue: str = "none", R=None, Y=None):
+    """``nmg_spmm_x16_epilogue``: Y = W_s X ("none") or W_s X + R ("add") from
+    prepared operands, the sum taken as the product is stored."""
+    _need_cuda(prepared, X)
+    if X.dtype != layout.dtype or X.shape[0] != layout.K:
+        raise ValueError("X must be K x N of the layout's dtype")
+    N = X.shape[1]
+    if Y is None:
+        Y = torch.empty((layout.M, N), dtype=X.dtype, device=X.device)
+    _need_cuda(Y)
+    if Y.dtype != layout.dtype or tuple(Y.shape) != (layout.M, N):
+        raise ValueError("Y must be M x N of the layout's dtype")
+    rp, ldr = ctypes.c_void_p(0), 0
+    if epilogue == "add":
+        if R is None:
+            raise ValueError("the add epilogue needs R")
+        _need_cuda(R)
+        if R.dtype != layout.dtype or tuple(R.shape) != (layout.M, N):
+            raise ValueError("R must be M x N of the layout's dtype")
+        rp, ldr = _ptr(R), _rows(R, "R")
+    _check(lib().nmg_spmm_x16_epilogue(ctypes.byref(layout.c), _ptr(prepared),
+                                       EPILOGUES[epilogue], _ptr(X), _rows(X, "X"), N, rp, ldr,
+                                       _ptr(Y), _rows(Y, "Y"), _stream(X)),
+           "nmg_spmm_x16_epilogue")
+    return Y
+
+
 def spmm_into(layout: Layout, values, indices, X, Y, kernel: str = "auto"):
     """``nmg_spmm_with`` into a caller-allocated Y (M x N); the families of
     X16_KERNELS go through ``nmg_x16_prepare`` + ``nmg_spmm_x16``."""
@@ -294,16 +323,13 @@ def spmm_epilogue(values, indices, X, layout: Layout, epilogue: str = "none", R=
     if Y.dtype != layout.dtype or tuple(Y.shape) != (layout.M, N):
         raise ValueError("Y must be M x N of the layout's dtype")
     if kernel in X16_KERNELS:
-        # the product, then the elementwise pass (no fused epilogue here)
-        P = spmm(values, indices, X, layout, kernel)
-        if epilogue == "gelu":
-            P = gelu(P)
-        elif epilogue == "add":
-            if R is None:
-                raise ValueError("the add epilogue needs R")
-            P = add(P, R.contiguous())
-        Y.copy_(P)
-        return Y
+        if X16_KERNELS[kernel] != layout.dtype:
+            raise NmgError(ERR_UNSUPPORTED, f"{kernel} takes {X16_KERNELS[kernel]}")
+        prepared = x16_prepare(values, indices, layout)
+        if epilogue != "gelu":           # the residual sum is fused into the product
+            return spmm_x16_epilogue(layout, prepared, X, epilogue, R, Y)
+        spmm_x16_epilogue(layout, prepared, X, "none", None, Y)
+        return gelu(Y, out=Y)
     rp, ldr = ctypes.c_void_p(0), 0
     if epilogue == "add":
         if R is None:

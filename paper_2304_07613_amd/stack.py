@@ -12,8 +12,13 @@ encoder block (without LayerNorm):
 Activations are features x tokens (768 x 4096), binary16 in memory, binary32
 inside every kernel.  Every step runs in libnmg's kernels; torch only holds
 the buffers.  By default GELU and the residual sums are folded into the
-products (``nmg_spmm_epilogue``); with a trace every step runs on its own so
-that each intermediate can be checked, and both give the same bits.
+products (``nmg_spmm_epilogue``, ``nmg_spmm_x16_epilogue``); with a trace
+every step runs on its own so that each intermediate can be checked, and both
+give the same bits.
+
+Each projection runs on a kernel family of its own (``kernels``, name ->
+family).  A family that works on prepared operands (``nmg.X16_KERNELS``) gets
+them once, when the stack is built, like the packing itself.
 """
 from __future__ import annotations
 
@@ -25,21 +30,33 @@ from . import synth
 
 NAMES = ("qkv", "ao", "up", "down")
 
+# the 16 x 16 x 32 binary16 product where its residual sum can ride along;
+# FFN up keeps the family that folds GELU into the product
+DEFAULT_KERNELS = {"qkv": "mfma_wide", "ao": "mfma_wide", "up": "auto", "down": "mfma_wide"}
+
 
 @dataclass
 class StackLayer:
     packed: dict = field(default_factory=dict)   # name -> (values, indices, layout)
     dense: dict = field(default_factory=dict)    # name -> dense weight (kept on request)
+    prepared: dict = field(default_factory=dict)  # name -> prepared operands (x16 families)
 
 
 class LinearStack:
-    def __init__(self, nmg, layers):
+    def __init__(self, nmg, layers, kernels=None):
         self.nmg = nmg
         self.layers = layers
+        self.kernels = dict.fromkeys(NAMES, "auto") if kernels is None else dict(kernels)
+        for layer in layers:
+            for name, kernel in self.kernels.items():
+                if kernel in nmg.X16_KERNELS and name not in layer.prepared:
+                    v, idx, L = layer.packed[name]
+                    layer.prepared[name] = nmg.x16_prepare(v, idx, L)
 
     @classmethod
     def from_workload(cls, workload: int, nmg, n=2, m=8, g=8, n_layers=synth.BERT_LAYERS,
-                      tokens=synth.BERT_TOKENS, keep_dense=True, device="cuda:0"):
+                      tokens=synth.BERT_TOKENS, keep_dense=True, device="cuda:0",
+                      kernels=DEFAULT_KERNELS):
         lins = synth.bert_stack_layers(tokens, n, m, g)
         layers = []
         for li in range(n_layers):
@@ -51,18 +68,22 @@ class LinearStack:
                 if keep_dense:
                     layer.dense[lin.name] = W
             layers.append(layer)
-        return cls(nmg, layers)
+        return cls(nmg, layers, kernels)
 
-    def linear(self, layer: StackLayer, name: str, x: torch.Tensor, out=None):
+    def linear(self, layer: StackLayer, name: str, x: torch.Tensor):
         v, idx, L = layer.packed[name]
-        if out is None:
-            return self.nmg.spmm(v, idx, x, L)
-        self.nmg.spmm_into(L, v, idx, x, out)
-        return out
+        if name in layer.prepared:
+            return self.nmg.spmm_x16_epilogue(L, layer.prepared[name], x)
+        return self.nmg.spmm(v, idx, x, L, self.kernels[name])
 
     def fused(self, layer: StackLayer, name: str, x: torch.Tensor, epilogue: str, r=None):
         v, idx, L = layer.packed[name]
-        return self.nmg.spmm_epilogue(v, idx, x, L, epilogue, r)
+        if name in layer.prepared:
+            if epilogue == "gelu":
+                p = self.linear(layer, name, x)
+                return self.nmg.gelu(p, out=p)
+            return self.nmg.spmm_x16_epilogue(L, layer.prepared[name], x, epilogue, r)
+        return self.nmg.spmm_epilogue(v, idx, x, L, epilogue, r, self.kernels[name])
 
     def forward_layer(self, layer: StackLayer, x: torch.Tensor, trace: dict | None = None):
         nmg = self.nmg

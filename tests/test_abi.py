@@ -171,3 +171,35 @@ def test_chunked_layout_validation(lib):
     assert lib.nmg_p_refine(ctypes.byref(L), p, 16, p, None, s) == nmg.ERR_NULL
     bad = nmg._PLayout(48, 16, 2, 4, 2, 6, 10, 4, nmg.F16)   # S inconsistent with P * g
     assert lib.nmg_p_compress(ctypes.byref(bad), p, 16, p, p, s) == nmg.ERR_PARAM
+
+
+def test_x16_validation(lib):
+    L = nmg._Layout()
+    p, s = ctypes.c_void_p(1 << 20), ctypes.c_void_p(0)
+    big = ctypes.c_void_p(1 << 30)
+    assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 2, 8, 8, nmg.F16) == nmg.OK
+    nbytes = lib.nmg_x16_prepared_bytes(ctypes.byref(L))
+    assert nbytes > 0 and nbytes % 16 == 0
+    assert lib.nmg_x16_prepare(ctypes.byref(L), p, None, p, s) == nmg.ERR_NULL
+    assert lib.nmg_x16_prepare(ctypes.byref(L), p, p, ctypes.c_void_p((1 << 20) + 8),
+                               s) == nmg.ERR_ALIGN
+    # only the prepared-operand entry points run these families
+    for fam in ("mfma_wide", "mfma_split"):
+        assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS[fam], p, p, p, 32, 32, p, 32,
+                                 s) == nmg.ERR_UNSUPPORTED
+    ep = lib.nmg_spmm_x16_epilogue
+    assert ep(ctypes.byref(L), p, 7, p, 64, 64, None, 0, big, 64, s) == nmg.ERR_PARAM   # epilogue
+    assert ep(ctypes.byref(L), p, 1, p, 64, 64, None, 0, big, 64, s) == nmg.ERR_UNSUPPORTED  # GELU
+    assert ep(ctypes.byref(L), p, 2, p, 64, 64, None, 64, big, 64, s) == nmg.ERR_NULL   # no R
+    assert ep(ctypes.byref(L), p, 2, p, 64, 64, big, 32, big, 64, s) == nmg.ERR_PARAM   # ldr < N
+    assert ep(ctypes.byref(L), p, 2, p, 64, 64, ctypes.c_void_p((1 << 30) + 8), 64,
+              p, 64, s) == nmg.ERR_UNSUPPORTED                                             # R 8-aligned
+    assert ep(ctypes.byref(L), p, 2, p, 64, 64, big, 64, big, 64, s) == nmg.ERR_PARAM   # R == Y
+    assert ep(ctypes.byref(L), p, 0, p, 64, 60, None, 0, big, 64, s) == nmg.ERR_UNSUPPORTED  # N % 8
+    assert lib.nmg_spmm_x16(ctypes.byref(L), p, p, 32, 64, big, 64, s) == nmg.ERR_PARAM  # ldx < N
+    # n = 3 and g % 8 != 0: not taken
+    assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 3, 8, 8, nmg.F16) == nmg.OK
+    assert lib.nmg_x16_prepared_bytes(ctypes.byref(L)) == -1
+    assert lib.nmg_x16_prepare(ctypes.byref(L), p, p, p, s) == nmg.ERR_UNSUPPORTED
+    assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 2, 8, 4, nmg.F32) == nmg.OK
+    assert lib.nmg_x16_prepared_bytes(ctypes.byref(L)) == -1

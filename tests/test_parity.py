@@ -310,7 +310,9 @@ def test_repack(nmg, M, K, n, m, g, dtype):
 @pytest.mark.parametrize("M,K,N,n,m,g,dtype", [
     (264, 72, 264, 2, 8, 8, torch.float16), (768, 768, 4096, 2, 8, 8, torch.float16),
     (3072, 768, 512, 2, 8, 8, torch.float16), (96, 48, 77, 2, 4, 12, torch.float16),
-    (128, 100, 136, 1, 10, 4, torch.float32), (64, 40, 33, 3, 8, 2, torch.float32)])
+    (128, 100, 136, 1, 10, 4, torch.float32), (64, 40, 33, 3, 8, 2, torch.float32),
+    (200, 64, 96, 1, 4, 8, torch.float16), (272, 96, 136, 2, 4, 16, torch.float32),
+    (136, 40, 260, 1, 4, 8, torch.float32)])
 def test_spmm_epilogue_equals_composition(nmg, M, K, N, n, m, g, dtype):
     """GELU / residual folded into the product give the bits of the product
     followed by nmg_gelu / nmg_add, for every kernel family that takes the
@@ -340,6 +342,21 @@ def test_spmm_epilogue_equals_composition(nmg, M, K, N, n, m, g, dtype):
     Ys = nmg.spmm_epilogue(v, idx, X, L, "add", Rb[:, :N], Y=Yb[:, :N])
     torch.cuda.synchronize()
     assert torch.equal(Ys.view(torch.uint8), nmg.add(nmg.spmm(v, idx, X, L), R).view(torch.uint8))
+    assert (Yb[:, N:] == 0).all()
+    # the same through prepared operands, when these products take the layout
+    x16 = "mfma_wide" if dtype == torch.float16 else "mfma_split"
+    try:
+        prepared = nmg.x16_prepare(v, idx, L)
+    except nmg.NmgError as e:
+        assert e.status == nmg.ERR_UNSUPPORTED
+        return
+    if N % (8 if dtype == torch.float16 else 4):
+        return
+    Yb.zero_()
+    Ys = nmg.spmm_x16_epilogue(L, prepared, X, "add", Rb[:, :N], Y=Yb[:, :N])
+    torch.cuda.synchronize()
+    assert torch.equal(Ys.view(torch.uint8),
+                       nmg.add(nmg.spmm(v, idx, X, L, x16), R).view(torch.uint8))
     assert (Yb[:, N:] == 0).all()
 
 
