@@ -72,7 +72,9 @@ typedef enum nmg_status {
     NMG_ERR_DTYPE = 4,       /* unknown element type                           */
     NMG_ERR_ALIGN = 5,       /* a pointer or leading dimension is misaligned   */
     NMG_ERR_LAUNCH = 6,      /* the HIP runtime reported an error on launch    */
-    NMG_ERR_UNSUPPORTED = 7  /* the requested kernel cannot run this layout    */
+    NMG_ERR_UNSUPPORTED = 7, /* the requested kernel cannot run this layout    */
+    NMG_ERR_CAPACITY = 8     /* a fixed-size working buffer is too small for
+                                the layout                                    */
 } nmg_status;
 
 typedef enum nmg_dtype {
@@ -130,14 +132,14 @@ typedef enum nmg_kernel {
     NMG_KERNEL_MFMA_WIDE = 9,    /* binary16 layouts on the 16 x 16 x 32
                                     binary16 matrix instruction (32 gathered
                                     k-slots of a group per instruction, binary32
-                                    accumulation); runs only through
-                                    nmg_spmm_x16 on prepared operands
-                                    (nmg_spmm_with returns
-                                    NMG_ERR_UNSUPPORTED)                      */
+                                    accumulation) from prepared operands: made
+                                    on every call by nmg_spmm_with, once per
+                                    weight with nmg_x16_prepare +
+                                    nmg_spmm_x16; the layouts and arguments
+                                    nmg_spmm_x16 takes                        */
     NMG_KERNEL_MFMA_SPLIT = 10   /* binary32 layouts on the same binary16
                                     instruction, each operand carried as two
-                                    binary16 parts; runs only through
-                                    nmg_spmm_x16 (see there)                  */
+                                    binary16 parts (see nmg_spmm_x16)         */
 } nmg_kernel;
 /* With n == m every column is kept and every index row is 0 .. m-1, so the
  * matrix-core kernels treat the weight as one group whatever g is. */
@@ -182,7 +184,10 @@ nmg_status nmg_spmm(const nmg_layout *layout, const void *values,
                     int64_t N, void *Y, int64_t ldy, hipStream_t stream);
 
 /* nmg_spmm with an explicit kernel family; NMG_ERR_UNSUPPORTED when that
- * family cannot run this layout. */
+ * family cannot run this layout.  NMG_KERNEL_MFMA_WIDE and
+ * NMG_KERNEL_MFMA_SPLIT make the prepared operands on every call, in device
+ * memory allocated and freed in stream order on `stream` (hipMallocAsync /
+ * hipFreeAsync; NMG_ERR_LAUNCH when the allocation fails). */
 nmg_status nmg_spmm_with(const nmg_layout *layout, nmg_kernel kernel,
                          const void *values, const uint8_t *indices,
                          const void *X, int64_t ldx, int64_t N, void *Y,
@@ -199,8 +204,9 @@ typedef enum nmg_epilogue {
 
 /* nmg_spmm_with followed by an epilogue; the result equals nmg_spmm_with
  * followed by nmg_gelu or nmg_add bit for bit.  NMG_KERNEL_MFMA_F16 and
- * NMG_KERNEL_SMFMAC_F16 apply the epilogue in the product kernel (no second pass over Y); the other
- * families run the elementwise kernel on Y afterwards.  R (ADD only; ignored
+ * NMG_KERNEL_SMFMAC_F16 apply the epilogue in the product kernel (no second pass over Y), and so
+ * do NMG_KERNEL_MFMA_WIDE / _SPLIT for ADD when R and ldr sit on 16-byte
+ * boundaries; the other cases run the elementwise kernel on Y afterwards.  R (ADD only; ignored
  * otherwise, may be NULL) is M x N with leading dimension ldr >= N, the
  * layout's element type, element-aligned, and must not overlap Y. */
 nmg_status nmg_spmm_epilogue(const nmg_layout *layout, nmg_kernel kernel, nmg_epilogue epilogue,

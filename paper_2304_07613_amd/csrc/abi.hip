@@ -163,6 +163,28 @@ nmg_status nmg_spmm_epilogue(const nmg_layout *L, nmg_kernel kernel, nmg_epilogu
                              const void *values, const uint8_t *indices, const void *X,
                              int64_t ldx, int64_t N, const void *R, int64_t ldr, void *Y,
                              int64_t ldy, hipStream_t stream) {
+    return spmm_epilogue_ws(L, kernel, epi, values, indices, X, ldx, N, R, ldr, Y, ldy, stream,
+                            nullptr, 0);
+}
+
+}  // extern "C"
+
+const nmg_layout *nmg_internal::effective_layout(const nmg_layout *L, nmg_layout *tmp) {
+    // n == m keeps every column, so every index row is 0 .. m-1: the whole
+    // weight is one group and the grouped kernels apply whatever g is
+    if (L->n == L->m && L->g != L->M) {
+        *tmp = *L;
+        tmp->g = L->M;
+        return tmp;
+    }
+    return L;
+}
+
+nmg_status nmg_internal::spmm_epilogue_ws(const nmg_layout *L, nmg_kernel kernel, nmg_epilogue epi,
+                                          const void *values, const uint8_t *indices,
+                                          const void *X, int64_t ldx, int64_t N, const void *R,
+                                          int64_t ldr, void *Y, int64_t ldy, hipStream_t stream,
+                                          void *workspace, int64_t workspace_bytes) {
     nmg_status st = check_layout(L);
     if (st != NMG_OK) return st;
     if (!values || !indices || !X || !Y) return NMG_ERR_NULL;
@@ -181,14 +203,8 @@ nmg_status nmg_spmm_epilogue(const nmg_layout *L, nmg_kernel kernel, nmg_epilogu
         const uintptr_t y1 = y0 + (uintptr_t)(((int64_t)(L->M - 1) * ldy + N) * (int64_t)es);
         if (r0 < y1 && y0 < r1) return NMG_ERR_PARAM;
     }
-    // n == m keeps every column, so every index row is 0 .. m-1: the whole
-    // weight is one group and the grouped kernels apply whatever g is
     nmg_layout dense;
-    if (L->n == L->m && L->g != L->M) {
-        dense = *L;
-        dense.g = L->M;
-        L = &dense;
-    }
+    L = effective_layout(L, &dense);
     prelaunch();
     SpmmArgs a{L, values, indices, X, ldx, (int)N, Y, ldy, stream};
     const bool half_ok = spmm_half_supported(L, X, ldx, N);
@@ -237,8 +253,30 @@ nmg_status nmg_spmm_epilogue(const nmg_layout *L, nmg_kernel kernel, nmg_epilogu
             st = spmm_valu_staged(a);
             break;
         case NMG_KERNEL_MFMA_WIDE:
-        case NMG_KERNEL_MFMA_SPLIT:
-            return NMG_ERR_UNSUPPORTED;  // these run on prepared operands only
+        case NMG_KERNEL_MFMA_SPLIT: {
+            if ((kernel == NMG_KERNEL_MFMA_SPLIT) != (L->dtype == NMG_F32) ||
+                !x16_args_supported(L, X, ldx, Y, ldy, N))
+                return NMG_ERR_UNSUPPORTED;
+            // the prepared operands live for this call only: in the caller's
+            // workspace, else in a stream-ordered allocation
+            const int64_t bytes = x16_prepared_bytes(L);
+            void *prepared = workspace;
+            if (workspace) {
+                if (bytes > workspace_bytes) return NMG_ERR_CAPACITY;
+            } else if (hipMallocAsync(&prepared, (size_t)bytes, stream) != hipSuccess) {
+                (void)hipGetLastError();
+                return NMG_ERR_LAUNCH;
+            }
+            const bool fuse = epi == NMG_EPILOGUE_ADD && x16_residual_supported(L, R, ldr);
+            st = x16_prepare(L, values, indices, prepared, stream);
+            if (st == NMG_OK)
+                st = x16_product(L, prepared, X, ldx, (int)N, Y, ldy,
+                                 fuse ? NMG_EPILOGUE_ADD : NMG_EPILOGUE_NONE, R, ldr, stream);
+            if (!workspace && hipFreeAsync(prepared, stream) != hipSuccess && st == NMG_OK)
+                st = NMG_ERR_LAUNCH;
+            if (fuse) return st;
+            break;
+        }
         default:
             return NMG_ERR_PARAM;
     }
@@ -256,6 +294,8 @@ nmg_status nmg_spmm_epilogue(const nmg_layout *L, nmg_kernel kernel, nmg_epilogu
     }
     return NMG_OK;
 }
+
+extern "C" {
 
 nmg_status nmg_p_layout_init(nmg_p_layout *layout, int32_t M, int32_t K, int32_t n, int32_t m,
                              int32_t g, nmg_dtype dtype) {
@@ -373,9 +413,7 @@ nmg_status nmg_spmm_x16_epilogue(const nmg_layout *L, const void *prepared, nmg_
     if (epi == NMG_EPILOGUE_ADD) {
         if (!R) return NMG_ERR_NULL;
         if (ldr < N) return NMG_ERR_PARAM;
-        // R is read 16 bytes at a time, on Y's pattern
-        if (!aligned(R, 16) || ldr % (16 / (int64_t)elem_size(L->dtype)) != 0)
-            return NMG_ERR_UNSUPPORTED;
+        if (!x16_residual_supported(L, R, ldr)) return NMG_ERR_UNSUPPORTED;
         const size_t es = elem_size(L->dtype);
         const uintptr_t r0 = reinterpret_cast<uintptr_t>(R), y0 = reinterpret_cast<uintptr_t>(Y);
         const uintptr_t r1 = r0 + (uintptr_t)(((int64_t)(L->M - 1) * ldr + N) * (int64_t)es);
@@ -438,6 +476,7 @@ const char *nmg_status_str(nmg_status s) {
         case NMG_ERR_ALIGN: return "misaligned pointer or leading dimension";
         case NMG_ERR_LAUNCH: return "kernel launch failed";
         case NMG_ERR_UNSUPPORTED: return "kernel does not support this layout";
+        case NMG_ERR_CAPACITY: return "layout exceeds a fixed-size working buffer";
     }
     return "unknown status";
 }

@@ -119,6 +119,21 @@ bool spmm_half_supported(const nmg_layout *L, const void *X, int64_t ldx, int64_
 // the 16 x 16 x 32 products (k_spmm_x16.hip): layout and argument checks,
 // size of the prepared operands, preparation and product
 bool x16_layout_supported(const nmg_layout *L);
+// the layout the kernels run: n == m keeps every column, so every index row
+// is 0 .. m-1 and the whole weight is one group (g = M); else L itself
+const nmg_layout *effective_layout(const nmg_layout *L, nmg_layout *tmp);
+// nmg_spmm_epilogue; the 16 x 16 x 32 families put their prepared operands
+// into `workspace` (NMG_ERR_CAPACITY when they need more than workspace_bytes),
+// or into a stream-ordered allocation when workspace is NULL
+nmg_status spmm_epilogue_ws(const nmg_layout *L, nmg_kernel kernel, nmg_epilogue epi,
+                            const void *values, const uint8_t *indices, const void *X, int64_t ldx,
+                            int64_t N, const void *R, int64_t ldr, void *Y, int64_t ldy,
+                            hipStream_t stream, void *workspace, int64_t workspace_bytes);
+// the fused residual sum of the 16 x 16 x 32 products reads R 16 bytes at a time
+inline bool x16_residual_supported(const nmg_layout *L, const void *R, int64_t ldr) {
+    const int64_t es = L->dtype == NMG_F32 ? 4 : 2;
+    return aligned(R, 16) && ldr % (16 / es) == 0;
+}
 bool x16_args_supported(const nmg_layout *L, const void *X, int64_t ldx, const void *Y,
                         int64_t ldy, int64_t N);
 int64_t x16_prepared_bytes(const nmg_layout *L);

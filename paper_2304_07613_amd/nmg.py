@@ -27,7 +27,8 @@ KERNELS = {"auto": 0, "valu": 1, "mfma": 2, "mfma_general": 3, "mfma_scalar": 4,
 _KERNEL_NAME = {v: k for k, v in KERNELS.items()}
 EPILOGUES = {"none": 0, "gelu": 1, "add": 2}
 
-OK, ERR_NULL, ERR_PARAM, ERR_SHAPE, ERR_DTYPE, ERR_ALIGN, ERR_LAUNCH, ERR_UNSUPPORTED = range(8)
+OK, ERR_NULL, ERR_PARAM, ERR_SHAPE, ERR_DTYPE, ERR_ALIGN, ERR_LAUNCH, ERR_UNSUPPORTED, ERR_CAPACITY = \
+    range(9)
 
 
 class NmgError(RuntimeError):
@@ -219,8 +220,9 @@ def repack(W: torch.Tensor, indices: torch.Tensor, layout: Layout) -> torch.Tens
     return values
 
 
-# kernel families that run on prepared operands (nmg_x16_prepare +
-# nmg_spmm_x16), and the element type each takes
+# kernel families that run on prepared operands (made per call by
+# nmg_spmm_with, or once by nmg_x16_prepare for nmg_spmm_x16), and the element
+# type each takes
 X16_KERNELS = {"mfma_wide": torch.float16, "mfma_split": torch.float32}
 
 
@@ -275,14 +277,8 @@ def spmm_x16_epilogue(layout: Layout, prepared, X, epilogue: str = "none", R=Non
 
 
 def spmm_into(layout: Layout, values, indices, X, Y, kernel: str = "auto"):
-    """``nmg_spmm_with`` into a caller-allocated Y (M x N); the families of
-    X16_KERNELS go through ``nmg_x16_prepare`` + ``nmg_spmm_x16``."""
+    """``nmg_spmm_with`` into a caller-allocated Y (M x N)."""
     _need_cuda(values, indices, X, Y)
-    if kernel in X16_KERNELS:
-        if X16_KERNELS[kernel] != layout.dtype:
-            raise NmgError(ERR_UNSUPPORTED, f"{kernel} takes {X16_KERNELS[kernel]}")
-        spmm_x16_into(layout, x16_prepare(values, indices, layout), X, Y)
-        return
     if X.dtype != layout.dtype or Y.dtype != layout.dtype or values.dtype != layout.dtype:
         raise TypeError("dtype mismatch")
     if X.shape[0] != layout.K or Y.shape[0] != layout.M or Y.shape[1] != X.shape[1]:
@@ -307,6 +303,10 @@ def spmm_epilogue(values, indices, X, layout: Layout, epilogue: str = "none", R=
                   kernel: str = "auto", Y=None):
     """Y = epilogue(W_s X): "none", "gelu" (GELU of the product) or "add"
     (product + R), bit for bit what spmm followed by gelu or add gives."""
+    return _spmm_epilogue("nmg_spmm_epilogue", values, indices, X, layout, epilogue, R, kernel, Y)
+
+
+def _spmm_epilogue(fn, values, indices, X, layout, epilogue, R, kernel, Y):
     _need_cuda(values, indices, X)
     if X.dtype != layout.dtype or values.dtype != layout.dtype:
         raise TypeError("dtype mismatch")
@@ -322,14 +322,6 @@ def spmm_epilogue(values, indices, X, layout: Layout, epilogue: str = "none", R=
     _need_cuda(Y)
     if Y.dtype != layout.dtype or tuple(Y.shape) != (layout.M, N):
         raise ValueError("Y must be M x N of the layout's dtype")
-    if kernel in X16_KERNELS:
-        if X16_KERNELS[kernel] != layout.dtype:
-            raise NmgError(ERR_UNSUPPORTED, f"{kernel} takes {X16_KERNELS[kernel]}")
-        prepared = x16_prepare(values, indices, layout)
-        if epilogue != "gelu":           # the residual sum is fused into the product
-            return spmm_x16_epilogue(layout, prepared, X, epilogue, R, Y)
-        spmm_x16_epilogue(layout, prepared, X, "none", None, Y)
-        return gelu(Y, out=Y)
     rp, ldr = ctypes.c_void_p(0), 0
     if epilogue == "add":
         if R is None:
@@ -338,9 +330,9 @@ def spmm_epilogue(values, indices, X, layout: Layout, epilogue: str = "none", R=
         if R.dtype != layout.dtype or tuple(R.shape) != (layout.M, N):
             raise ValueError("R must be M x N of the layout's dtype")
         rp, ldr = _ptr(R), _rows(R, "R")
-    _check(lib().nmg_spmm_epilogue(ctypes.byref(layout.c), KERNELS[kernel], EPILOGUES[epilogue],
-                                   _ptr(values), _ptr(indices), _ptr(X), _rows(X, "X"), N, rp,
-                                   ldr, _ptr(Y), _rows(Y, "Y"), _stream(X)), "nmg_spmm_epilogue")
+    _check(getattr(lib(), fn)(ctypes.byref(layout.c), KERNELS[kernel], EPILOGUES[epilogue],
+                              _ptr(values), _ptr(indices), _ptr(X), _rows(X, "X"), N, rp, ldr,
+                              _ptr(Y), _rows(Y, "Y"), _stream(X)), fn)
     return Y
 
 

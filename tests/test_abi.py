@@ -132,7 +132,7 @@ def test_calls_reject_bad_arguments_before_launch(lib):
 
 
 def test_status_strings(lib):
-    for st in range(8):
+    for st in range(9):
         assert nmg.status_str(st)
     assert nmg.status_str(99) == "unknown status"
 
@@ -183,10 +183,12 @@ def test_x16_validation(lib):
     assert lib.nmg_x16_prepare(ctypes.byref(L), p, None, p, s) == nmg.ERR_NULL
     assert lib.nmg_x16_prepare(ctypes.byref(L), p, p, ctypes.c_void_p((1 << 20) + 8),
                                s) == nmg.ERR_ALIGN
-    # only the prepared-operand entry points run these families
-    for fam in ("mfma_wide", "mfma_split"):
-        assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS[fam], p, p, p, 32, 32, p, 32,
-                                 s) == nmg.ERR_UNSUPPORTED
+    # the binary32 family declines binary16; N % 8 != 0 is declined (before
+    # any allocation)
+    assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS["mfma_split"], p, p, p, 32, 32, big,
+                             32, s) == nmg.ERR_UNSUPPORTED
+    assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS["mfma_wide"], p, p, p, 36, 36, big,
+                             36, s) == nmg.ERR_UNSUPPORTED
     ep = lib.nmg_spmm_x16_epilogue
     assert ep(ctypes.byref(L), p, 7, p, 64, 64, None, 0, big, 64, s) == nmg.ERR_PARAM   # epilogue
     assert ep(ctypes.byref(L), p, 1, p, 64, 64, None, 0, big, 64, s) == nmg.ERR_UNSUPPORTED  # GELU
