@@ -214,6 +214,23 @@ nmg_status nmg_spmm_epilogue(const nmg_layout *layout, nmg_kernel kernel, nmg_ep
                              int64_t ldx, int64_t N, const void *R, int64_t ldr, void *Y,
                              int64_t ldy, hipStream_t stream);
 
+/* nmg_spmm_epilogue for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): same arguments, same results bit for bit, and no allocation.
+ * NMG_KERNEL_MFMA_WIDE / _SPLIT put their prepared operands into a fixed
+ * 16 MiB array in device memory instead of a stream-ordered allocation (one
+ * array per GPU, held until the process ends; NMG_ERR_CAPACITY for a layout
+ * whose prepared operands, nmg_x16_prepared_bytes, exceed it).  Every call on
+ * a GPU shares that GPU's array: calls that overlap on one GPU (from several
+ * threads or on several streams) race, so serialise them.  `stream` must
+ * belong to the current device (NMG_ERR_PARAM).  The other families use no
+ * scratch memory and run exactly as in nmg_spmm_epilogue. */
+nmg_status nmg_spmm_epilogue_noalloc(const nmg_layout *layout, nmg_kernel kernel,
+                                     nmg_epilogue epilogue, const void *values,
+                                     const uint8_t *indices, const void *X, int64_t ldx,
+                                     int64_t N, const void *R, int64_t ldr, void *Y,
+                                     int64_t ldy, hipStream_t stream);
+
 /* The kernel family NMG_KERNEL_AUTO picks for this layout and N, assuming
  * 16-byte aligned X, 4-byte aligned indices and ldx = N (never
  * NMG_KERNEL_MFMA; NMG_KERNEL_AUTO only for an invalid layout). */

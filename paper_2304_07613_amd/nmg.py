@@ -81,6 +81,8 @@ def lib():
         "nmg_spmm_with": ([lp, ctypes.c_int, vp, vp, vp, i64, i64, vp, i64, vp], ctypes.c_int),
         "nmg_spmm_epilogue": ([lp, ctypes.c_int, ctypes.c_int, vp, vp, vp, i64, i64, vp, i64, vp,
                                i64, vp], ctypes.c_int),
+        "nmg_spmm_epilogue_noalloc": ([lp, ctypes.c_int, ctypes.c_int, vp, vp, vp, i64, i64, vp,
+                                       i64, vp, i64, vp], ctypes.c_int),
         "nmg_spmm_auto_kernel": ([lp, i64], ctypes.c_int),
         "nmg_densify": ([lp, vp, vp, vp, i64, vp], ctypes.c_int),
         "nmg_gelu": ([ctypes.c_int, vp, vp, i64, vp], ctypes.c_int),
@@ -304,6 +306,16 @@ def spmm_epilogue(values, indices, X, layout: Layout, epilogue: str = "none", R=
     """Y = epilogue(W_s X): "none", "gelu" (GELU of the product) or "add"
     (product + R), bit for bit what spmm followed by gelu or add gives."""
     return _spmm_epilogue("nmg_spmm_epilogue", values, indices, X, layout, epilogue, R, kernel, Y)
+
+
+def spmm_epilogue_noalloc(values, indices, X, layout: Layout, epilogue: str = "none", R=None,
+                          kernel: str = "auto", Y=None):
+    """``nmg_spmm_epilogue_noalloc``: spmm_epilogue without device allocation
+    in the library (the prepared operands of mfma_wide / mfma_split go to the
+    library's fixed per-GPU array; overlapping calls on one GPU race).  Y is
+    allocated here when not given: pass Y to allocate nothing at all."""
+    return _spmm_epilogue("nmg_spmm_epilogue_noalloc", values, indices, X, layout, epilogue, R,
+                          kernel, Y)
 
 
 def _spmm_epilogue(fn, values, indices, X, layout, epilogue, R, kernel, Y):

@@ -205,3 +205,22 @@ def test_x16_validation(lib):
     assert lib.nmg_x16_prepare(ctypes.byref(L), p, p, p, s) == nmg.ERR_UNSUPPORTED
     assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 2, 8, 4, nmg.F32) == nmg.OK
     assert lib.nmg_x16_prepared_bytes(ctypes.byref(L)) == -1
+
+
+def test_noalloc_refuses_before_launch(lib):
+    """The allocation-free product refuses a layout whose prepared operands
+    exceed its fixed array, and bad arguments, on the host."""
+    L = nmg._Layout()
+    p, s = ctypes.c_void_p(1 << 20), ctypes.c_void_p(0)
+    assert lib.nmg_layout_init(ctypes.byref(L), 32768, 8192, 2, 8, 8, nmg.F16) == nmg.OK
+    assert lib.nmg_x16_prepared_bytes(ctypes.byref(L)) > 16 << 20
+    na = lib.nmg_spmm_epilogue_noalloc
+    assert na(ctypes.byref(L), nmg.KERNELS["mfma_wide"], 0, p, p, p, 4096, 4096, None, 0, p,
+              4096, s) == nmg.ERR_CAPACITY
+    assert na(ctypes.byref(L), nmg.KERNELS["mfma_wide"], 0, None, p, p, 4096, 4096, None, 0, p,
+              4096, s) == nmg.ERR_NULL
+    assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 3, 8, 8, nmg.F16) == nmg.OK
+    assert na(ctypes.byref(L), nmg.KERNELS["mfma_wide"], 0, p, p, p, 64, 64, None, 0, p, 64,
+              s) == nmg.ERR_UNSUPPORTED
+    # the other families take nmg_spmm_epilogue's path and its checks
+    assert na(ctypes.byref(L), 0, 7, p, p, p, 64, 64, None, 0, p, 64, s) == nmg.ERR_PARAM
