@@ -50,7 +50,8 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "spmm_bert-ffn-up_traffic.txt")
 KERNEL_SYMBOL = {"mfma_scalar": "k_spmm_mfma_s", "mfma_general": "k_spmm_mfma",
                  "mfma_f16": "k_spmm_mfma_h", "mfma_direct": "k_spmm_mfma_d",
                  "smfmac_f16": "k_spmm_smfmac", "valu_staged": "k_spmm_valu_s",
-                 "valu": "k_spmm_valu", "mfma_wide": "k_spmm_x16", "mfma_split": "k_spmm_x16"}
+                 "valu": "k_spmm_valu", "mfma_wide": "k_spmm_x16", "mfma_split": "k_spmm_x16",
+                 "mfma_expand": "k_spmm_mfma_s"}
 
 
 def parse():
@@ -60,7 +61,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=1000)
     ap.add_argument("--kernel", choices=("auto", "mfma", "valu", "mfma_general", "mfma_scalar",
                                          "mfma_f16", "mfma_direct", "smfmac_f16",
-                                         "valu_staged", "mfma_wide", "mfma_split"),
+                                         "valu_staged", "mfma_wide", "mfma_split",
+                                         "mfma_expand"),
                     default="auto")
     ap.add_argument("--workload", type=int, choices=(1, 2, 3), default=2)
     ap.add_argument("--sweep", action="store_true")
@@ -220,7 +222,7 @@ def family_times(ctx, L, sets, kernel, reps=20):
     torch, nmg = ctx.torch, ctx.nmg
     out = {}
     for fam in ("smfmac_f16", "mfma_f16", "mfma_wide", "mfma_direct", "mfma_scalar",
-                "mfma_general", "mfma_split", "valu_staged", "valu"):
+                "mfma_general", "mfma_split", "mfma_expand", "valu_staged", "valu"):
         try:
             for r in range(3):
                 W, X, v, idx, Y = sets[r % len(sets)]

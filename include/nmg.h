@@ -137,9 +137,20 @@ typedef enum nmg_kernel {
                                     weight with nmg_x16_prepare +
                                     nmg_spmm_x16; the layouts and arguments
                                     nmg_spmm_x16 takes                        */
-    NMG_KERNEL_MFMA_SPLIT = 10   /* binary32 layouts on the same binary16
+    NMG_KERNEL_MFMA_SPLIT = 10,  /* binary32 layouts on the same binary16
                                     instruction, each operand carried as two
                                     binary16 parts (see nmg_spmm_x16)         */
+    NMG_KERNEL_MFMA_EXPAND = 11  /* the matrix cores for groups they cannot
+                                    share (g % 4 != 0, n not a power of two):
+                                    W_s written out dense (zeros elsewhere)
+                                    into scratch memory (M K elements + K
+                                    bytes, stream-ordered on every call), then
+                                    multiplied as one dense group by the
+                                    MFMA_SCALAR kernel -- m / n times the
+                                    useful work, and a non-finite X entry
+                                    reaches every output of its token, as in a
+                                    dense product; needs M % 4 == 0 and
+                                    M K < 2^31                               */
 } nmg_kernel;
 /* With n == m every column is kept and every index row is 0 .. m-1, so the
  * matrix-core kernels treat the weight as one group whatever g is. */
@@ -178,16 +189,19 @@ nmg_status nmg_repack(const nmg_layout *layout, const void *W, int64_t ldw,
  * element by element, more slowly.  `indices` must hold n
  * strictly ascending in-chunk offsets per (group, chunk), as nmg_compress
  * writes them; other contents are not detected and give unspecified Y (the
- * kernels still never read outside X's K rows).  Uses NMG_KERNEL_AUTO. */
+ * kernels still never read outside X's K rows).  Uses NMG_KERNEL_AUTO, which
+ * takes NMG_KERNEL_MFMA_EXPAND (scratch memory in stream order, dense-product
+ * treatment of non-finite X) for binary32 layouts the grouped matrix-core
+ * kernels cannot take when m <= 8 n. */
 nmg_status nmg_spmm(const nmg_layout *layout, const void *values,
                     const uint8_t *indices, const void *X, int64_t ldx,
                     int64_t N, void *Y, int64_t ldy, hipStream_t stream);
 
 /* nmg_spmm with an explicit kernel family; NMG_ERR_UNSUPPORTED when that
- * family cannot run this layout.  NMG_KERNEL_MFMA_WIDE and
- * NMG_KERNEL_MFMA_SPLIT make the prepared operands on every call, in device
- * memory allocated and freed in stream order on `stream` (hipMallocAsync /
- * hipFreeAsync; NMG_ERR_LAUNCH when the allocation fails). */
+ * family cannot run this layout.  NMG_KERNEL_MFMA_WIDE / _SPLIT (prepared
+ * operands) and NMG_KERNEL_MFMA_EXPAND (the dense weight) keep their scratch
+ * memory in device memory allocated and freed in stream order on `stream`
+ * (hipMallocAsync / hipFreeAsync; NMG_ERR_LAUNCH when the allocation fails). */
 nmg_status nmg_spmm_with(const nmg_layout *layout, nmg_kernel kernel,
                          const void *values, const uint8_t *indices,
                          const void *X, int64_t ldx, int64_t N, void *Y,
@@ -217,10 +231,12 @@ nmg_status nmg_spmm_epilogue(const nmg_layout *layout, nmg_kernel kernel, nmg_ep
 /* nmg_spmm_epilogue for callers that cannot allocate device memory (code
  * under HIP graph capture, tight serving loops, harnesses that forbid
  * allocation): same arguments, same results bit for bit, and no allocation.
- * NMG_KERNEL_MFMA_WIDE / _SPLIT put their prepared operands into a fixed
- * 16 MiB array in device memory instead of a stream-ordered allocation (one
- * array per GPU, held until the process ends; NMG_ERR_CAPACITY for a layout
- * whose prepared operands, nmg_x16_prepared_bytes, exceed it).  Every call on
+ * The families with scratch memory (NMG_KERNEL_MFMA_WIDE / _SPLIT, their
+ * prepared operands; NMG_KERNEL_MFMA_EXPAND, chosen explicitly or by
+ * NMG_KERNEL_AUTO, the dense weight) keep it in a fixed 16 MiB array in
+ * device memory instead of a stream-ordered allocation (one array per GPU,
+ * held until the process ends; NMG_ERR_CAPACITY for a layout whose scratch
+ * memory -- nmg_x16_prepared_bytes, or M K elements + K bytes -- exceeds it).  Every call on
  * a GPU shares that GPU's array: calls that overlap on one GPU (from several
  * threads or on several streams) race, so serialise them.  `stream` must
  * belong to the current device (NMG_ERR_PARAM).  The other families use no

@@ -149,6 +149,7 @@ nmg_kernel nmg_spmm_auto_kernel(const nmg_layout *L, int64_t N) {
     if (spmm_direct_preferred(L, N, N)) return NMG_KERNEL_MFMA_DIRECT;
     if (spmm_scalar_supported(L, nullptr, N)) return NMG_KERNEL_MFMA_SCALAR;
     if (spmm_general_supported(L, N)) return NMG_KERNEL_MFMA_GENERAL;
+    if (expand_preferred(L, N)) return NMG_KERNEL_MFMA_EXPAND;
     return spmm_valu_staged_preferred(L, nullptr, N, N) ? NMG_KERNEL_VALU_STAGED : NMG_KERNEL_VALU;
 }
 
@@ -164,10 +165,65 @@ nmg_status nmg_spmm_epilogue(const nmg_layout *L, nmg_kernel kernel, nmg_epilogu
                              int64_t ldx, int64_t N, const void *R, int64_t ldr, void *Y,
                              int64_t ldy, hipStream_t stream) {
     return spmm_epilogue_ws(L, kernel, epi, values, indices, X, ldx, N, R, ldr, Y, ldy, stream,
-                            nullptr, 0);
+                            nullptr);
 }
 
 }  // extern "C"
+
+namespace {
+
+// The expanded weight as a layout: one group, chunks of one column, every
+// column kept (its index bytes are all 0)
+nmg_layout expanded_layout(const nmg_layout *L) {
+    nmg_layout D = *L;
+    D.n = 1;
+    D.m = 1;
+    D.g = L->M;
+    D.C = L->K;
+    return D;
+}
+
+constexpr int64_t round256(int64_t b) { return (b + 255) / 256 * 256; }
+
+// Scratch memory from the caller's source, else in stream order
+void *take_scratch(scratch_source src, int64_t bytes, hipStream_t stream, nmg_status *st) {
+    if (src) return src(bytes, stream, st);
+    void *p = nullptr;
+    if (hipMallocAsync(&p, (size_t)bytes, stream) != hipSuccess || p == nullptr) {
+        (void)hipGetLastError();
+        *st = NMG_ERR_LAUNCH;
+        return nullptr;
+    }
+    return p;
+}
+
+nmg_status give_back_scratch(scratch_source src, void *p, hipStream_t stream, nmg_status st) {
+    if (!src && hipFreeAsync(p, stream) != hipSuccess) {
+        (void)hipGetLastError();
+        if (st == NMG_OK) st = NMG_ERR_LAUNCH;
+    }
+    return st;
+}
+
+}  // namespace
+
+// AUTO's binary32 choice among the families for groups the grouped
+// matrix-core kernels cannot share: the expanded product does m / n times
+// the useful work at the matrix rate, the staged vector kernel the useful
+// work at about a seventh of it (measured break-even near m / n = 10)
+bool nmg_internal::expand_preferred(const nmg_layout *L, int64_t ldx) {
+    return L->dtype == NMG_F32 && L->m <= 8 * L->n && expand_supported(L, ldx);
+}
+
+int64_t nmg_internal::expand_scratch_bytes(const nmg_layout *L) {
+    return round256((int64_t)L->M * L->K * (int64_t)elem_size(L->dtype)) + round256(L->K);
+}
+
+bool nmg_internal::expand_supported(const nmg_layout *L, int64_t ldx) {
+    if ((int64_t)L->M * L->K >= ((int64_t)1 << 31)) return false;
+    const nmg_layout D = expanded_layout(L);
+    return check_layout(&D) == NMG_OK && spmm_scalar_supported(&D, nullptr, ldx);
+}
 
 const nmg_layout *nmg_internal::effective_layout(const nmg_layout *L, nmg_layout *tmp) {
     // n == m keeps every column, so every index row is 0 .. m-1: the whole
@@ -184,7 +240,7 @@ nmg_status nmg_internal::spmm_epilogue_ws(const nmg_layout *L, nmg_kernel kernel
                                           const void *values, const uint8_t *indices,
                                           const void *X, int64_t ldx, int64_t N, const void *R,
                                           int64_t ldr, void *Y, int64_t ldy, hipStream_t stream,
-                                          void *workspace, int64_t workspace_bytes) {
+                                          scratch_source scratch) {
     nmg_status st = check_layout(L);
     if (st != NMG_OK) return st;
     if (!values || !indices || !X || !Y) return NMG_ERR_NULL;
@@ -217,6 +273,7 @@ nmg_status nmg_internal::spmm_epilogue_ws(const nmg_layout *L, nmg_kernel kernel
                  : scalar_ok ? NMG_KERNEL_MFMA_SCALAR
                  : spmm_general_supported(L, N) || kernel == NMG_KERNEL_MFMA
                      ? NMG_KERNEL_MFMA_GENERAL
+                 : expand_preferred(L, ldx) ? NMG_KERNEL_MFMA_EXPAND
                  : spmm_valu_staged_preferred(L, X, ldx, N) ? NMG_KERNEL_VALU_STAGED
                                                               : NMG_KERNEL_VALU;
     }
@@ -257,25 +314,32 @@ nmg_status nmg_internal::spmm_epilogue_ws(const nmg_layout *L, nmg_kernel kernel
             if ((kernel == NMG_KERNEL_MFMA_SPLIT) != (L->dtype == NMG_F32) ||
                 !x16_args_supported(L, X, ldx, Y, ldy, N))
                 return NMG_ERR_UNSUPPORTED;
-            // the prepared operands live for this call only: in the caller's
-            // workspace, else in a stream-ordered allocation
-            const int64_t bytes = x16_prepared_bytes(L);
-            void *prepared = workspace;
-            if (workspace) {
-                if (bytes > workspace_bytes) return NMG_ERR_CAPACITY;
-            } else if (hipMallocAsync(&prepared, (size_t)bytes, stream) != hipSuccess) {
-                (void)hipGetLastError();
-                return NMG_ERR_LAUNCH;
-            }
+            // the prepared operands live for this call only
+            void *prepared = take_scratch(scratch, x16_prepared_bytes(L), stream, &st);
+            if (!prepared) return st;
             const bool fuse = epi == NMG_EPILOGUE_ADD && x16_residual_supported(L, R, ldr);
             st = x16_prepare(L, values, indices, prepared, stream);
             if (st == NMG_OK)
                 st = x16_product(L, prepared, X, ldx, (int)N, Y, ldy,
                                  fuse ? NMG_EPILOGUE_ADD : NMG_EPILOGUE_NONE, R, ldr, stream);
-            if (!workspace && hipFreeAsync(prepared, stream) != hipSuccess && st == NMG_OK)
-                st = NMG_ERR_LAUNCH;
+            st = give_back_scratch(scratch, prepared, stream, st);
             if (fuse) return st;
             break;
+        }
+        case NMG_KERNEL_MFMA_EXPAND: {
+            if (!expand_supported(L, ldx)) return NMG_ERR_UNSUPPORTED;
+            // the dense weight and its index bytes live for this call only
+            void *ws = take_scratch(scratch, expand_scratch_bytes(L), stream, &st);
+            if (!ws) return st;
+            const nmg_layout D = expanded_layout(L);
+            char *wd = static_cast<char *>(ws);
+            uint8_t *zi = reinterpret_cast<uint8_t *>(
+                wd + round256((int64_t)L->M * L->K * (int64_t)es));
+            st = launch_densify(L, values, indices, wd, L->K, stream, zi);
+            if (st == NMG_OK)  // the epilogue goes with the dense product
+                st = spmm_epilogue_ws(&D, NMG_KERNEL_MFMA_SCALAR, epi, wd, zi, X, ldx, N, R, ldr,
+                                      Y, ldy, stream, scratch);
+            return give_back_scratch(scratch, ws, stream, st);
         }
         default:
             return NMG_ERR_PARAM;

@@ -2,16 +2,18 @@
 // allocate device memory (code under HIP graph capture, serving loops,
 // harnesses that forbid allocation).
 //
-// The only scratch memory of the library's products is the prepared operands
-// that the 16 x 16 x 32 families (NMG_KERNEL_MFMA_WIDE / _SPLIT) make from
-// the packed weight on every nmg_spmm_epilogue call, there in a stream-ordered
-// allocation.  Here they go to one fixed array in device memory instead, a
-// copy of it on every GPU the library runs on, held until the process ends.
-// The preparation writes every byte of the region it uses before the product
-// reads it, so nothing has to be cleared between calls; calls that overlap on
-// one GPU (several host threads, or several streams) share the array and race.
-// The other families use no scratch memory and run as nmg_spmm_epilogue runs
-// them.
+// The library's products have scratch memory in two families: the prepared
+// operands that the 16 x 16 x 32 products (NMG_KERNEL_MFMA_WIDE / _SPLIT) make
+// from the packed weight, and the dense weight of the expanded product
+// (NMG_KERNEL_MFMA_EXPAND, also an NMG_KERNEL_AUTO choice), made on every
+// nmg_spmm_epilogue call in a stream-ordered allocation.  Here they go to one
+// fixed array in device memory instead, a copy of it on every GPU the library
+// runs on, held until the process ends.  Each family writes every byte of the
+// region it uses before reading it (the preparation, and the densify pass
+// that also zeroes the index bytes), so nothing has to be cleared between
+// calls; calls that overlap on one GPU (several host threads, or several
+// streams) share the array and race.  The other families use no scratch
+// memory and run as nmg_spmm_epilogue runs them.
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -50,38 +52,43 @@ void *scratch_address(int device) {
     return p;
 }
 
+
+// The scratch source of this entry point: the current device's array
+// (after checking that the work's stream is on that device), or
+// NMG_ERR_CAPACITY before any runtime call when the request exceeds it.
+void *fixed_scratch(int64_t bytes, hipStream_t stream, nmg_status *st) {
+    if (bytes > kScratchBytes) {
+        *st = NMG_ERR_CAPACITY;
+        return nullptr;
+    }
+    int device = -1, stream_device = -1;
+    if (hipGetDevice(&device) != hipSuccess || device < 0 || device >= kMaxDevices) {
+        (void)hipGetLastError();
+        *st = NMG_ERR_LAUNCH;
+        return nullptr;
+    }
+    if (stream != nullptr) {
+        if (hipStreamGetDevice(stream, &stream_device) != hipSuccess) {
+            (void)hipGetLastError();
+            *st = NMG_ERR_LAUNCH;
+            return nullptr;
+        }
+        if (stream_device != device) {
+            *st = NMG_ERR_PARAM;
+            return nullptr;
+        }
+    }
+    void *p = scratch_address(device);
+    if (!p) *st = NMG_ERR_LAUNCH;
+    return p;
+}
+
 }  // namespace
 
 nmg_status nmg_spmm_epilogue_noalloc(const nmg_layout *L, nmg_kernel kernel, nmg_epilogue epi,
                                      const void *values, const uint8_t *indices, const void *X,
                                      int64_t ldx, int64_t N, const void *R, int64_t ldr, void *Y,
                                      int64_t ldy, hipStream_t stream) {
-    if (kernel != NMG_KERNEL_MFMA_WIDE && kernel != NMG_KERNEL_MFMA_SPLIT)
-        return nmg_spmm_epilogue(L, kernel, epi, values, indices, X, ldx, N, R, ldr, Y, ldy,
-                                 stream);
-    nmg_status st = check_layout(L);
-    if (st != NMG_OK) return st;
-    if (!values || !indices || !X || !Y) return NMG_ERR_NULL;
-    // the size check comes before any runtime call
-    nmg_layout tmp;
-    const int64_t bytes = x16_prepared_bytes(effective_layout(L, &tmp));
-    if (bytes < 0) return NMG_ERR_UNSUPPORTED;
-    if (bytes > kScratchBytes) return NMG_ERR_CAPACITY;
-    // the array of the GPU the work runs on, which must be the current one
-    int device = -1, stream_device = -1;
-    if (hipGetDevice(&device) != hipSuccess || device < 0 || device >= kMaxDevices) {
-        (void)hipGetLastError();
-        return NMG_ERR_LAUNCH;
-    }
-    if (stream != nullptr) {
-        if (hipStreamGetDevice(stream, &stream_device) != hipSuccess) {
-            (void)hipGetLastError();
-            return NMG_ERR_LAUNCH;
-        }
-        if (stream_device != device) return NMG_ERR_PARAM;
-    }
-    void *ws = scratch_address(device);
-    if (!ws) return NMG_ERR_LAUNCH;
-    return spmm_epilogue_ws(L, kernel, epi, values, indices, X, ldx, N, R, ldr, Y, ldy, stream, ws,
-                            kScratchBytes);
+    return spmm_epilogue_ws(L, kernel, epi, values, indices, X, ldx, N, R, ldr, Y, ldy, stream,
+                            fixed_scratch);
 }

@@ -83,8 +83,10 @@ nmg_status launch_compress(const nmg_layout *L, const void *W, int64_t ldw, void
                            uint8_t *indices, hipStream_t stream);
 nmg_status launch_repack(const nmg_layout *L, const void *W, int64_t ldw, const uint8_t *indices,
                          void *values, hipStream_t stream);
+// `zeros` (may be NULL): K bytes set to 0 on the way (the index bytes of the
+// expanded weight's one-column chunks)
 nmg_status launch_densify(const nmg_layout *L, const void *values, const uint8_t *indices,
-                          void *W_out, int64_t ldw, hipStream_t stream);
+                          void *W_out, int64_t ldw, hipStream_t stream, uint8_t *zeros = nullptr);
 nmg_status launch_gelu(nmg_dtype dtype, const void *in, void *out, int64_t count,
                        hipStream_t stream);
 nmg_status launch_add(nmg_dtype dtype, const void *a, const void *b, void *out, int64_t count,
@@ -122,13 +124,25 @@ bool x16_layout_supported(const nmg_layout *L);
 // the layout the kernels run: n == m keeps every column, so every index row
 // is 0 .. m-1 and the whole weight is one group (g = M); else L itself
 const nmg_layout *effective_layout(const nmg_layout *L, nmg_layout *tmp);
-// nmg_spmm_epilogue; the 16 x 16 x 32 families put their prepared operands
-// into `workspace` (NMG_ERR_CAPACITY when they need more than workspace_bytes),
-// or into a stream-ordered allocation when workspace is NULL
+// Where a product's scratch memory comes from: a function that returns
+// `bytes` of device memory that is the call's alone until its work on the
+// stream is done, or NULL with *st set (NMG_ERR_CAPACITY when the request is
+// too large for it).
+typedef void *(*scratch_source)(int64_t bytes, hipStream_t stream, nmg_status *st);
+// nmg_spmm_epilogue; the families with scratch memory (the 16 x 16 x 32
+// products' prepared operands, the expanded weight) take it from `scratch`,
+// or from a stream-ordered allocation when scratch is NULL
 nmg_status spmm_epilogue_ws(const nmg_layout *L, nmg_kernel kernel, nmg_epilogue epi,
                             const void *values, const uint8_t *indices, const void *X, int64_t ldx,
                             int64_t N, const void *R, int64_t ldr, void *Y, int64_t ldy,
-                            hipStream_t stream, void *workspace, int64_t workspace_bytes);
+                            hipStream_t stream, scratch_source scratch);
+// The expanded product: W_s written out dense (zeros elsewhere) as a layout
+// of one group with one-column chunks, multiplied by the binary32 /
+// widened-binary16 matrix-core kernel.  Scratch bytes it needs; whether it
+// takes the layout.
+int64_t expand_scratch_bytes(const nmg_layout *L);
+bool expand_supported(const nmg_layout *L, int64_t ldx);
+bool expand_preferred(const nmg_layout *L, int64_t ldx);
 // the fused residual sum of the 16 x 16 x 32 products reads R 16 bytes at a time
 inline bool x16_residual_supported(const nmg_layout *L, const void *R, int64_t ldr) {
     const int64_t es = L->dtype == NMG_F32 ? 4 : 2;

@@ -9,7 +9,8 @@
 //               (group, chunk) pairs): binary32 group score down the g rows,
 //               rank by counting inside the chunk through LDS, then a
 //               coalesced copy of the kept weights.
-//   k_densify   one thread per output element.
+//   k_densify   one thread per output element (k_densify_chunks: one per
+//               chunk, for chunks of 4 or 8 columns).
 //   k_repack    one thread per kept slot: values from W at given indices.
 #include "common.hpp"
 
@@ -309,11 +310,13 @@ __global__ __launch_bounds__(kBlock) void k_compress_chunk(
 template <typename T>
 __global__ __launch_bounds__(kBlock) void k_densify(
     const T *__restrict__ values, const uint8_t *__restrict__ indices,
-    T *__restrict__ out, int64_t ldw, int K, int n, int m, int g, int C) {
+    T *__restrict__ out, int64_t ldw, int K, int n, int m, int g, int C,
+    uint8_t *__restrict__ zeros) {
     using B = typename Bits<T>::type;
     const int64_t r = blockIdx.x;
     const int k = blockIdx.y * kBlock + threadIdx.x;
     if (k >= K) return;
+    if (zeros != nullptr && r == 0) zeros[k] = 0;  // the expanded weight's index bytes
     const int c = k / m, o = k - c * m;
     const int64_t ldv = (int64_t)C * n;
     const uint8_t *idx = indices + (r / g) * ldv + (int64_t)c * n;
@@ -321,6 +324,37 @@ __global__ __launch_bounds__(kBlock) void k_densify(
     for (int s = 0; s < n; ++s)
         if (idx[s] == o) v = reinterpret_cast<const B *>(values)[r * ldv + (int64_t)c * n + s];
     reinterpret_cast<B *>(out)[r * ldw + k] = v;
+}
+
+// The same for layouts whose chunks are all MV columns wide: one thread per
+// (row, chunk) writes the chunk's MV outputs in one vector store (the
+// expanded product's densify pass writes M K elements at the store rate)
+template <typename T, int MV>
+__global__ __launch_bounds__(kBlock) void k_densify_chunks(
+    const T *__restrict__ values, const uint8_t *__restrict__ indices,
+    T *__restrict__ out, int64_t ldw, int n, int g, int C, uint8_t *__restrict__ zeros) {
+    using B = typename Bits<T>::type;
+    typedef B VB __attribute__((ext_vector_type(MV)));
+    const int64_t r = blockIdx.x;
+    const int c = blockIdx.y * kBlock + threadIdx.x;
+    if (c >= C) return;
+    const int64_t ldv = (int64_t)C * n;
+    const uint8_t *idx = indices + (r / g) * ldv + (int64_t)c * n;
+    const B *val = reinterpret_cast<const B *>(values) + r * ldv + (int64_t)c * n;
+    VB o;
+#pragma unroll
+    for (int j = 0; j < MV; ++j) o[j] = 0;
+    for (int s = 0; s < n; ++s) {  // a later slot with the same offset wins, as in k_densify
+        const int off = idx[s];
+        const B v = val[s];
+#pragma unroll
+        for (int j = 0; j < MV; ++j)
+            if (off == j) o[j] = v;
+    }
+    if (zeros != nullptr && r == 0)
+#pragma unroll
+        for (int j = 0; j < MV; ++j) zeros[(int64_t)c * MV + j] = 0;
+    *reinterpret_cast<VB *>(reinterpret_cast<B *>(out) + r * ldw + (int64_t)c * MV) = o;
 }
 
 // Fixed-mask repack: one thread per kept slot of a row; the offset is clamped
@@ -398,15 +432,33 @@ nmg_status launch_compress(const nmg_layout *L, const void *W, int64_t ldw, void
 }
 
 nmg_status launch_densify(const nmg_layout *L, const void *values, const uint8_t *indices,
-                          void *W_out, int64_t ldw, hipStream_t stream) {
+                          void *W_out, int64_t ldw, hipStream_t stream, uint8_t *zeros) {
+    const int64_t es = (int64_t)elem_size(L->dtype);
+    const int64_t vb = L->m * es;  // bytes of one chunk's vector store
+    if ((L->m == 4 || L->m == 8) && L->K % L->m == 0 && (vb & (vb - 1)) == 0 &&
+        aligned(W_out, (size_t)vb) && (ldw * es) % vb == 0) {
+        dim3 grid(L->M, (L->C + kBlock - 1) / kBlock);
+#define NMG_DENSIFY_CHUNKS(T, MV)                                                             \
+    hipLaunchKernelGGL((k_densify_chunks<T, MV>), grid, dim3(kBlock), 0, stream,             \
+                       (const T *)values, indices, (T *)W_out, ldw, L->n, L->g, L->C, zeros)
+        if (L->dtype == NMG_F32) {
+            if (L->m == 4) NMG_DENSIFY_CHUNKS(float, 4);
+            else NMG_DENSIFY_CHUNKS(float, 8);
+        } else {
+            if (L->m == 4) NMG_DENSIFY_CHUNKS(_Float16, 4);
+            else NMG_DENSIFY_CHUNKS(_Float16, 8);
+        }
+#undef NMG_DENSIFY_CHUNKS
+        return launched();
+    }
     dim3 grid(L->M, (L->K + kBlock - 1) / kBlock);
     if (L->dtype == NMG_F32)
         hipLaunchKernelGGL((k_densify<float>), grid, dim3(kBlock), 0, stream, (const float *)values,
-                           indices, (float *)W_out, ldw, L->K, L->n, L->m, L->g, L->C);
+                           indices, (float *)W_out, ldw, L->K, L->n, L->m, L->g, L->C, zeros);
     else
         hipLaunchKernelGGL((k_densify<_Float16>), grid, dim3(kBlock), 0, stream,
                            (const _Float16 *)values, indices, (_Float16 *)W_out, ldw, L->K, L->n,
-                           L->m, L->g, L->C);
+                           L->m, L->g, L->C, zeros);
     return launched();
 }
 

@@ -23,7 +23,8 @@ LIB_PATH = _build.LIB_PATH
 F32, F16 = 0, 1
 _DTYPE_CODE = {torch.float32: F32, torch.float16: F16}
 KERNELS = {"auto": 0, "valu": 1, "mfma": 2, "mfma_general": 3, "mfma_scalar": 4, "mfma_f16": 5,
-           "mfma_direct": 6, "smfmac_f16": 7, "valu_staged": 8, "mfma_wide": 9, "mfma_split": 10}
+           "mfma_direct": 6, "smfmac_f16": 7, "valu_staged": 8, "mfma_wide": 9, "mfma_split": 10,
+           "mfma_expand": 11}
 _KERNEL_NAME = {v: k for k, v in KERNELS.items()}
 EPILOGUES = {"none": 0, "gelu": 1, "add": 2}
 

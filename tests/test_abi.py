@@ -72,12 +72,21 @@ def test_calls_reject_bad_arguments_before_launch(lib):
     assert lib.nmg_gelu(nmg.F32, p, p, 0, s) == nmg.OK   # empty input: nothing to launch
     bad = nmg._Layout(64, 64, 1, 4, 8, 17, nmg.F32)    # inconsistent C
     assert lib.nmg_compress(ctypes.byref(bad), p, 64, p, p, s) == nmg.ERR_PARAM
-    # g % 4 != 0: the matrix-core kernels decline, a vector kernel is the choice
-    # (the LDS-staged one when X rows can be copied 16 bytes at a time)
+    # g % 4 != 0: the grouped matrix-core kernels decline; at m <= 8 n the
+    # expanded dense weight on the matrix cores is the choice
     assert lib.nmg_layout_init(ctypes.byref(L), 64, 64, 1, 4, 2, nmg.F32) == nmg.OK
     for fam in ("mfma", "mfma_general", "mfma_scalar", "mfma_f16", "mfma_direct", "smfmac_f16"):
         assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS[fam], p, p, p, 32, 32, p, 32,
                                  s) == nmg.ERR_UNSUPPORTED
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 32) == nmg.KERNELS["mfma_expand"]
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 30) == nmg.KERNELS["mfma_expand"]
+    # M % 4 != 0: no expanded product either
+    assert lib.nmg_layout_init(ctypes.byref(L), 66, 64, 1, 4, 2, nmg.F32) == nmg.OK
+    assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS["mfma_expand"], p, p, p, 32, 32, p, 32,
+                             s) == nmg.ERR_UNSUPPORTED
+    # above m = 8 n a vector kernel is the choice (the LDS-staged one when X
+    # rows can be copied 16 bytes at a time)
+    assert lib.nmg_layout_init(ctypes.byref(L), 64, 640, 1, 10, 2, nmg.F32) == nmg.OK
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 32) == nmg.KERNELS["valu_staged"]
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 30) == nmg.KERNELS["valu"]    # N % 4 != 0
     assert lib.nmg_layout_init(ctypes.byref(L), 64, 660, 1, 33, 1, nmg.F32) == nmg.OK
@@ -98,9 +107,14 @@ def test_calls_reject_bad_arguments_before_launch(lib):
     # a layer too small to fill the GPU without splitting its k-slots
     assert lib.nmg_layout_init(ctypes.byref(L), 768, 768, 2, 4, 4, nmg.F32) == nmg.OK
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 128) == nmg.KERNELS["mfma_direct"]
-    # n = 3 is not a power of two: the general matrix-core kernel declines too
+    # n = 3 is not a power of two: the general matrix-core kernel declines too,
+    # the expanded product takes it
     assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 3, 8, 8, nmg.F32) == nmg.OK
-    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["valu_staged"]
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_expand"]
+    # binary32 g = 1 sweep points: expanded at 2:4, 1:4, 2:8; staged vector FMAs at 1:10
+    for n_, m_ in ((2, 4), (1, 4), (2, 8)):
+        assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, n_, m_, 1, nmg.F32) == nmg.OK
+        assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_expand"]
     # n = m (dense) with g = 1: one group, so the matrix cores take it
     assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 4, 4, 1, nmg.F32) == nmg.OK
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_scalar"]

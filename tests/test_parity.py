@@ -105,7 +105,7 @@ def spmm_full(nmg, v, idx, L, X, rv, ridx, kernel, tag=""):
 
 # every kernel family; the matrix-core ones decline layouts they cannot take
 KERNELS = ["auto", "valu", "mfma_general", "mfma_scalar", "mfma_f16", "mfma_direct", "smfmac_f16",
-           "valu_staged", "mfma_wide", "mfma_split"]
+           "valu_staged", "mfma_wide", "mfma_split", "mfma_expand"]
 
 
 def kernels_for(nmg, L, N):

@@ -1,7 +1,9 @@
 """nmg_spmm_epilogue_noalloc against nmg_spmm_epilogue, through the C ABI.
 
-The allocation-free entry point keeps the prepared operands of the 16 x 16 x
-32 families in the library's fixed per-GPU array; its results must equal the
+The allocation-free entry point keeps the scratch memory of the families that
+have some (the 16 x 16 x 32 products' prepared operands, the expanded
+product's dense weight, also when AUTO picks it) in the library's fixed
+per-GPU array; its results must equal the
 allocating entry point's bit for bit (same kernels), on consecutive calls
 that reuse the array, the second with a smaller layout (whatever the first
 left in the array must not leak into it).
@@ -45,6 +47,8 @@ CASES = [
     ("mfma_wide", torch.float16, (768, 3072, 1024, 1, 4, 16), (200, 64, 96, 1, 4, 8)),
     ("mfma_split", torch.float32, (768, 3072, 2048, 1, 4, 8), (136, 40, 260, 1, 4, 8)),
     ("mfma_split", torch.float32, (1024, 512, 512, 2, 4, 16), (272, 96, 136, 2, 4, 16)),
+    ("mfma_expand", torch.float32, (3072, 768, 1024, 2, 4, 1), (200, 64, 96, 1, 4, 2)),
+    ("auto", torch.float32, (1024, 768, 512, 3, 8, 8), (64, 40, 33, 3, 8, 2)),
 ]
 
 
