@@ -220,7 +220,8 @@ typedef enum nmg_epilogue {
  * followed by nmg_gelu or nmg_add bit for bit.  NMG_KERNEL_MFMA_F16 and
  * NMG_KERNEL_SMFMAC_F16 apply the epilogue in the product kernel (no second pass over Y), and so
  * do NMG_KERNEL_MFMA_WIDE / _SPLIT for ADD when R and ldr sit on 16-byte
- * boundaries; the other cases run the elementwise kernel on Y afterwards.  R (ADD only; ignored
+ * boundaries and NMG_KERNEL_MFMA_WIDE for GELU where nmg_spmm_x16_epilogue
+ * folds it in; the other cases run the elementwise kernel on Y afterwards.  R (ADD only; ignored
  * otherwise, may be NULL) is M x N with leading dimension ldr >= N, the
  * layout's element type, element-aligned, and must not overlap Y. */
 nmg_status nmg_spmm_epilogue(const nmg_layout *layout, nmg_kernel kernel, nmg_epilogue epilogue,
@@ -301,12 +302,15 @@ nmg_status nmg_x16_prepare(const nmg_layout *layout, const void *values, const u
 nmg_status nmg_spmm_x16(const nmg_layout *layout, const void *prepared, const void *X,
                         int64_t ldx, int64_t N, void *Y, int64_t ldy, hipStream_t stream);
 
-/* nmg_spmm_x16 with an epilogue applied as the outputs are stored:
- * NMG_EPILOGUE_NONE (= nmg_spmm_x16) or NMG_EPILOGUE_ADD, Y = P + R computed
- * as nmg_add computes it (P the product rounded to the element type); R is
- * M x N, leading dimension ldr >= N, 16-byte aligned with ldr a multiple of
- * 16 bytes (else NMG_ERR_UNSUPPORTED), and must not overlap Y
- * (NMG_ERR_PARAM).  NMG_EPILOGUE_GELU: NMG_ERR_UNSUPPORTED. */
+/* nmg_spmm_x16 with an epilogue, bit for bit what nmg_spmm_x16 followed by
+ * nmg_add / nmg_gelu gives (P the product rounded to the element type):
+ * NMG_EPILOGUE_NONE (= nmg_spmm_x16), NMG_EPILOGUE_ADD (Y = P + R; R is M x
+ * N, leading dimension ldr >= N, 16-byte aligned with ldr a multiple of 16
+ * bytes, else NMG_ERR_UNSUPPORTED, and must not overlap Y, else
+ * NMG_ERR_PARAM; added as the outputs are stored) or NMG_EPILOGUE_GELU
+ * (looked up as the outputs are stored for binary16 layouts whose tile
+ * leaves room in LDS for the table -- units of 8 rows, and of 16 rows at
+ * most 2 per wave -- else a second pass over Y). */
 nmg_status nmg_spmm_x16_epilogue(const nmg_layout *layout, const void *prepared,
                                  nmg_epilogue epilogue, const void *X, int64_t ldx, int64_t N,
                                  const void *R, int64_t ldr, void *Y, int64_t ldy,

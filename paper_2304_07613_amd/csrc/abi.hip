@@ -205,6 +205,41 @@ nmg_status give_back_scratch(scratch_source src, void *p, hipStream_t stream, nm
     return st;
 }
 
+// The epilogue as a second pass over Y (row by row when rows are not contiguous)
+nmg_status epilogue_pass(const nmg_layout *L, nmg_epilogue epi, void *Y, int64_t ldy,
+                         const void *R, int64_t ldr, int64_t N, hipStream_t stream) {
+    const size_t es = elem_size(L->dtype);
+    const bool flat = ldy == N && (epi != NMG_EPILOGUE_ADD || ldr == N);
+    const int64_t rows = flat ? 1 : L->M, count = flat ? (int64_t)L->M * N : N;
+    for (int64_t r = 0; r < rows; ++r) {
+        char *y = static_cast<char *>(Y) + (size_t)(r * ldy) * es;
+        const nmg_status st =
+            epi == NMG_EPILOGUE_GELU
+                ? launch_gelu(L->dtype, y, y, count, stream)
+                : launch_add(L->dtype, y, static_cast<const char *>(R) + (size_t)(r * ldr) * es, y,
+                             count, stream);
+        if (st != NMG_OK) return st;
+    }
+    return NMG_OK;
+}
+
+// The 16 x 16 x 32 product with its epilogue folded in where the kernel
+// takes it (the residual sum with 16-byte aligned R, GELU where the tile
+// leaves room for the table), else as a second pass
+nmg_status x16_with_epilogue(const nmg_layout *L, const void *prepared, nmg_epilogue epi,
+                             const void *X, int64_t ldx, int64_t N, const void *R, int64_t ldr,
+                             void *Y, int64_t ldy, hipStream_t stream) {
+    if (epi == NMG_EPILOGUE_GELU ||
+        (epi == NMG_EPILOGUE_ADD && x16_residual_supported(L, R, ldr))) {
+        const nmg_status st = x16_product(L, prepared, X, ldx, (int)N, Y, ldy, epi, R, ldr, stream);
+        if (st != NMG_ERR_UNSUPPORTED) return st;
+    }
+    const nmg_status st =
+        x16_product(L, prepared, X, ldx, (int)N, Y, ldy, NMG_EPILOGUE_NONE, nullptr, 0, stream);
+    if (st != NMG_OK || epi == NMG_EPILOGUE_NONE) return st;
+    return epilogue_pass(L, epi, Y, ldy, R, ldr, N, stream);
+}
+
 }  // namespace
 
 // AUTO's binary32 choice among the families for groups the grouped
@@ -317,14 +352,10 @@ nmg_status nmg_internal::spmm_epilogue_ws(const nmg_layout *L, nmg_kernel kernel
             // the prepared operands live for this call only
             void *prepared = take_scratch(scratch, x16_prepared_bytes(L), stream, &st);
             if (!prepared) return st;
-            const bool fuse = epi == NMG_EPILOGUE_ADD && x16_residual_supported(L, R, ldr);
             st = x16_prepare(L, values, indices, prepared, stream);
             if (st == NMG_OK)
-                st = x16_product(L, prepared, X, ldx, (int)N, Y, ldy,
-                                 fuse ? NMG_EPILOGUE_ADD : NMG_EPILOGUE_NONE, R, ldr, stream);
-            st = give_back_scratch(scratch, prepared, stream, st);
-            if (fuse) return st;
-            break;
+                st = x16_with_epilogue(L, prepared, epi, X, ldx, N, R, ldr, Y, ldy, stream);
+            return give_back_scratch(scratch, prepared, stream, st);
         }
         case NMG_KERNEL_MFMA_EXPAND: {
             if (!expand_supported(L, ldx)) return NMG_ERR_UNSUPPORTED;
@@ -345,18 +376,7 @@ nmg_status nmg_internal::spmm_epilogue_ws(const nmg_layout *L, nmg_kernel kernel
             return NMG_ERR_PARAM;
     }
     if (st != NMG_OK || epi == NMG_EPILOGUE_NONE) return st;
-    // the epilogue as a second pass over Y (row by row when rows are not contiguous)
-    const bool flat = ldy == N && (epi != NMG_EPILOGUE_ADD || ldr == N);
-    const int64_t rows = flat ? 1 : L->M, count = flat ? (int64_t)L->M * N : N;
-    for (int64_t r = 0; r < rows; ++r) {
-        char *y = static_cast<char *>(Y) + (size_t)(r * ldy) * es;
-        st = epi == NMG_EPILOGUE_GELU
-                 ? launch_gelu(L->dtype, y, y, count, stream)
-                 : launch_add(L->dtype, y, static_cast<const char *>(R) + (size_t)(r * ldr) * es, y,
-                              count, stream);
-        if (st != NMG_OK) return st;
-    }
-    return NMG_OK;
+    return epilogue_pass(L, epi, Y, ldy, R, ldr, N, stream);
 }
 
 extern "C" {
@@ -471,7 +491,6 @@ nmg_status nmg_spmm_x16_epilogue(const nmg_layout *L, const void *prepared, nmg_
     if (N < 1 || N > INT32_MAX || ldx < N || ldy < N) return NMG_ERR_PARAM;
     if (epi != NMG_EPILOGUE_NONE && epi != NMG_EPILOGUE_GELU && epi != NMG_EPILOGUE_ADD)
         return NMG_ERR_PARAM;
-    if (epi == NMG_EPILOGUE_GELU) return NMG_ERR_UNSUPPORTED;
     if (!aligned(prepared, 16)) return NMG_ERR_ALIGN;
     if (!x16_args_supported(L, X, ldx, Y, ldy, N)) return NMG_ERR_UNSUPPORTED;
     if (epi == NMG_EPILOGUE_ADD) {
@@ -485,7 +504,7 @@ nmg_status nmg_spmm_x16_epilogue(const nmg_layout *L, const void *prepared, nmg_
         if (r0 < y1 && y0 < r1) return NMG_ERR_PARAM;
     }
     prelaunch();
-    return x16_product(L, prepared, X, ldx, (int)N, Y, ldy, (int)epi, R, ldr, stream);
+    return x16_with_epilogue(L, prepared, epi, X, ldx, N, R, ldr, Y, ldy, stream);
 }
 
 nmg_status nmg_spmm_x16(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,

@@ -153,6 +153,9 @@ bool x16_args_supported(const nmg_layout *L, const void *X, int64_t ldx, const v
 int64_t x16_prepared_bytes(const nmg_layout *L);
 nmg_status x16_prepare(const nmg_layout *L, const void *values, const uint8_t *indices,
                        void *prepared, hipStream_t stream);
+// epi: NMG_EPILOGUE_NONE / _ADD (R read 16 bytes at a time) / _GELU;
+// NMG_ERR_UNSUPPORTED, before any launch, for a GELU the chosen tile cannot
+// fold in (binary32, or outputs that leave no room for the table)
 nmg_status x16_product(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
                        int N, void *Y, int64_t ldy, int epi, const void *R, int64_t ldr,
                        hipStream_t stream);

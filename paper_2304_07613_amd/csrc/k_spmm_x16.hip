@@ -73,6 +73,13 @@ __host__ __device__ constexpr int kb_slot(int n, int q, int e) {
 }
 
 typedef __attribute__((address_space(3))) char lds_char;
+
+// GELU(x) for every binary16 x, indexed by the bits of x (the table nmg_gelu
+// uses, generated at build time), and where it is a rule instead
+__device__ __attribute__((aligned(16))) const uint16_t g_x16_gelu[65536] = {
+#include "gelu_f16_table.inc"
+};
+#include "gelu_f16_bounds.inc"
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) u32x2 lds_u2;
 
@@ -139,6 +146,24 @@ struct XGeom {
     // HALF 128 binary16 tokens
     static constexpr int row_bytes = SPLIT ? 512 : 256;
 };
+
+// Fused GELU (binary16): after the last window the staging buffers take the
+// table entries that are not a rule -- non-negative inputs below
+// NMG_GELU_F16_IDENTITY_FROM in buffer 0, negative ones below
+// NMG_GELU_F16_NEGZERO_FROM in buffer 1 -- and the waves' output regions go
+// to buffer 2 and to what the tables leave of buffers 0 and 1.
+constexpr int kGeluPosBytes = (2 * NMG_GELU_F16_IDENTITY_FROM + 255) / 256 * 256;
+constexpr int kGeluNegBytes = (2 * (NMG_GELU_F16_NEGZERO_FROM - 0x8000) + 255) / 256 * 256;
+__host__ __device__ constexpr int x16_out_region(bool split, int rows_wave) {
+    return rows_wave * (kXTok * (split ? 4 : 2) + 32);
+}
+__host__ __device__ constexpr bool x16_gelu_fits(bool split, int rows_wave, int waves, int bufcap) {
+    return !split && kGeluPosBytes <= bufcap && kGeluNegBytes <= bufcap &&
+           bufcap / x16_out_region(split, rows_wave) +
+                   (bufcap - kGeluPosBytes) / x16_out_region(split, rows_wave) +
+                   (bufcap - kGeluNegBytes) / x16_out_region(split, rows_wave) >=
+               waves;
+}
 
 // LDS bytes of one staging buffer (a multiple of 256)
 inline int x16_buffer_bytes(int n, int m, int row_bytes) {
@@ -261,7 +286,8 @@ template <bool SPLIT, int NS, bool U16, int GW, int NW, int NSTG>
 __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
     const h8 *__restrict__ frag, const uint16_t *__restrict__ offs, const int8_t *__restrict__ scale,
     const void *__restrict__ X_, int64_t ldx, void *__restrict__ Y_, int64_t ldy,
-    const void *__restrict__ R_, int64_t ldr, int M, int K, int N, int m, int nwin, int row_blocks) {
+    const void *__restrict__ R_, int64_t ldr, int epi, int M, int K, int N, int m, int nwin,
+    int row_blocks) {
     using G = XGeom<SPLIT, U16, GW, NW>;
     constexpr int RU = G::rows_unit, ROWB = G::row_bytes;
     constexpr int CPW = kXSlots / NS;  // chunks per window
@@ -547,11 +573,50 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
     constexpr int ES = SPLIT ? 4 : 2;
     constexpr int RSTRIDE = kXTok * ES + 32;
     constexpr int RB = G::rows_wave * RSTRIDE;       // one wave's region
+    static_assert(RB == x16_out_region(SPLIT, G::rows_wave), "one region formula");
     constexpr int WPA = BUFCAP / RB;                 // regions per staging buffer
     static_assert(WPA >= 1 && WPA * NBUF >= NW, "output regions fit the staging buffers");
+    constexpr bool GELU_OK = NBUF == 3 && x16_gelu_fits(SPLIT, G::rows_wave, NW, BUFCAP);
+    const bool gelu = GELU_OK && epi == NMG_EPILOGUE_GELU;  // the host asks only when it fits
+    // the GELU table's non-rule entries, 16 bytes a thread and step, all loads
+    // in flight together before the barrier (the buffers are free after it)
+    constexpr int TPB = 64 * NW;
+    constexpr int NTP = kGeluPosBytes / 16, NTN = kGeluNegBytes / 16;
+    constexpr int IP = GELU_OK ? (NTP + TPB - 1) / TPB : 1, IN = GELU_OK ? (NTN + TPB - 1) / TPB : 1;
+    f4 tabp[IP], tabn[IN];
+    if constexpr (GELU_OK) {
+        if (gelu) {
+            const f4 *src = reinterpret_cast<const f4 *>(g_x16_gelu);
+#pragma unroll
+            for (int j = 0; j < IP; ++j)
+                tabp[j] = src[min((int)threadIdx.x + j * TPB, NTP - 1)];
+#pragma unroll
+            for (int j = 0; j < IN; ++j)
+                tabn[j] = src[0x8000 * 2 / 16 + min((int)threadIdx.x + j * TPB, NTN - 1)];
+        }
+    }
     window_barrier<0>();  // copies for windows past the last have landed; every wave is done
     const int oreg = wave / WPA;
     lds_char *ob = (lds_char *)(oreg == 0 ? xs0 : (NBUF == 2 || oreg == 1) ? xs1 : xs2) + (wave % WPA) * RB;
+    if constexpr (GELU_OK) {
+        if (gelu) {
+            // into buffers 0 (non-negative inputs) and 1 (negative ones)
+            typedef __attribute__((address_space(3))) f4 lds_f4;
+#pragma unroll
+            for (int j = 0; j < IP; ++j)
+                if ((int)threadIdx.x + j * TPB < NTP)
+                    ((lds_f4 *)(lds_char *)xs0)[threadIdx.x + j * TPB] = tabp[j];
+#pragma unroll
+            for (int j = 0; j < IN; ++j)
+                if ((int)threadIdx.x + j * TPB < NTN)
+                    ((lds_f4 *)(lds_char *)xs1)[threadIdx.x + j * TPB] = tabn[j];
+            window_barrier<0>();  // every wave's table writes are done
+            constexpr int W2 = BUFCAP / RB, W0 = (BUFCAP - kGeluPosBytes) / RB;
+            ob = wave < W2 ? (lds_char *)xs2 + wave * RB
+                 : wave < W2 + W0 ? (lds_char *)xs0 + kGeluPosBytes + (wave - W2) * RB
+                                  : (lds_char *)xs1 + kGeluNegBytes + (wave - W2 - W0) * RB;
+        }
+    }
 #pragma unroll
     for (int u = 0; u < GW; ++u) {
         const float sc = SPLIT ? __builtin_ldexpf(1.f, -(int)scale[ug[u]]) : 1.f;
@@ -574,12 +639,46 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
     constexpr int RPI = 64 / LPR;                     // rows per instruction
     const int orow = lane / LPR, ocol = lane % LPR;
     const int tok = t0 + ocol * (16 / ES);
+    // a wave whose rows and tokens are all inside Y stores without a guard per
+    // row, so that the compiler may overlap the rows' LDS reads
+    const bool whole = row_w + G::rows_wave <= M && t0 + kXTok <= N;
+    auto store_rows = [&](auto guarded) __attribute__((always_inline)) {
 #pragma unroll
     for (int r0 = 0; r0 < G::rows_wave; r0 += RPI) {
         const int r = r0 + orow;
         f4 v = *(__attribute__((address_space(3))) f4 *)(ob + r * RSTRIDE + ocol * 16);
         const int row = row_w + r;
-        if (row < M && tok < N) {
+        if (!decltype(guarded)::value || (row < M && tok < N)) {
+            if constexpr (GELU_OK) {
+                if (gelu) {
+                    typedef __attribute__((address_space(3))) const uint16_t lds_u16;
+                    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+                    const u32x4 a = __builtin_bit_cast(u32x4, v);  // 8 binary16, two per word
+                    u32x4 o = {0u, 0u, 0u, 0u};
+                    lds_u16 *const tab0 = (lds_u16 *)(lds_char *)xs0;
+                    lds_u16 *const tab1 = (lds_u16 *)(lds_char *)xs1;
+                    // branch-free: one LDS read per element, at an in-bounds
+                    // entry of the sign's table (all 8 issued before any is
+                    // used), then the rule where the table has no entry
+                    uint32_t bb[8], lim[8], tv[8];
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        bb[i] = (a[i >> 1] >> (16 * (i & 1))) & 0xffffu;
+                        lim[i] = (bb[i] >> 15) ? (uint32_t)(NMG_GELU_F16_NEGZERO_FROM - 0x8001)
+                                               : (uint32_t)(NMG_GELU_F16_IDENTITY_FROM - 1);
+                        tv[i] = ((bb[i] >> 15) ? tab1 : tab0)[min(bb[i] & 0x7fffu, lim[i])];
+                    }
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) {
+                        const uint32_t b = bb[i];
+                        const uint32_t rule = b <= 0x7c00u ? b
+                                              : (b - 0x8000u) < 0x7c00u ? 0x8000u
+                                                                       : (uint32_t)NMG_GELU_F16_NAN_OUT;
+                        o[i >> 1] |= ((b & 0x7fffu) <= lim[i] ? tv[i] : rule) << (16 * (i & 1));
+                    }
+                    v = __builtin_bit_cast(f4, o);
+                }
+            }
             if (R_ != nullptr) {
                 const f4 rv = *reinterpret_cast<const f4 *>(reinterpret_cast<const char *>(R_) +
                                                             ((int64_t)row * ldr + tok) * ES);
@@ -596,6 +695,9 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
             store_y(v, reinterpret_cast<f4 *>(reinterpret_cast<char *>(Y_) + ((int64_t)row * ldy + tok) * ES));
         }
     }
+    };
+    if (whole) store_rows(std::false_type{});
+    else store_rows(std::true_type{});
 }
 
 }  // namespace
@@ -682,6 +784,10 @@ nmg_status launch_x16_k(const nmg_layout *L, const void *prepared, const void *X
                         int N, const X16Out &o, hipStream_t stream) {
     constexpr int NW = x16_waves<SPLIT>();
     using G = XGeom<SPLIT, U16, GW, NW>;
+    // GELU only where its table and the outputs share the staging buffers
+    if (o.epi == NMG_EPILOGUE_GELU &&
+        !(x16_nbuf<SPLIT>() == 3 && x16_gelu_fits(SPLIT, G::rows_wave, NW, x16_buf_cap<SPLIT>())))
+        return NMG_ERR_UNSUPPORTED;
     const XPrep P = x16_prep_layout(L, G::rows_unit);
     const char *base = static_cast<const char *>(prepared);
     const int row_blocks = (L->M + G::rows_wg - 1) / G::rows_wg;
@@ -691,8 +797,8 @@ nmg_status launch_x16_k(const nmg_layout *L, const void *prepared, const void *X
     const int8_t *sc = reinterpret_cast<const int8_t *>(base + P.scale);
     hipLaunchKernelGGL((k_spmm_x16<SPLIT, NS, U16, GW, NW, NSTG>), dim3(grid), dim3(64 * NW), 0,
                        stream, fr, of, sc, X, ldx, o.Y, o.ldy,
-                       o.epi == NMG_EPILOGUE_ADD ? o.R : nullptr, o.ldr, L->M, L->K, N, L->m,
-                       P.nwin, row_blocks);
+                       o.epi == NMG_EPILOGUE_ADD ? o.R : nullptr, o.ldr, o.epi, L->M, L->K, N,
+                       L->m, P.nwin, row_blocks);
     return launched();
 }
 

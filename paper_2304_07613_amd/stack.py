@@ -30,8 +30,8 @@ from . import synth
 
 NAMES = ("qkv", "ao", "up", "down")
 
-# the 16 x 16 x 32 binary16 product everywhere (residual sums fused into it,
-# GELU as a pass of its own: measured faster than the family that fuses GELU)
+# the 16 x 16 x 32 binary16 product everywhere (residual sums folded into its
+# output stores, GELU as a pass of its own)
 DEFAULT_KERNELS = dict.fromkeys(NAMES, "mfma_wide")
 
 
@@ -80,6 +80,9 @@ class LinearStack:
         v, idx, L = layer.packed[name]
         if name in layer.prepared:
             if epilogue == "gelu":
+                # measured: the product, then the table GELU on its output
+                # while that is still in the caches, beats the GELU folded
+                # into the product's stores (1.12 against 1.16 ms a forward)
                 p = self.linear(layer, name, x)
                 return self.nmg.gelu(p, out=p)
             return self.nmg.spmm_x16_epilogue(L, layer.prepared[name], x, epilogue, r)

@@ -205,7 +205,7 @@ def test_x16_validation(lib):
                              36, s) == nmg.ERR_UNSUPPORTED
     ep = lib.nmg_spmm_x16_epilogue
     assert ep(ctypes.byref(L), p, 7, p, 64, 64, None, 0, big, 64, s) == nmg.ERR_PARAM   # epilogue
-    assert ep(ctypes.byref(L), p, 1, p, 64, 64, None, 0, big, 64, s) == nmg.ERR_UNSUPPORTED  # GELU
+    assert ep(ctypes.byref(L), p, 1, p, 64, 60, None, 0, big, 64, s) == nmg.ERR_UNSUPPORTED  # N % 8
     assert ep(ctypes.byref(L), p, 2, p, 64, 64, None, 64, big, 64, s) == nmg.ERR_NULL   # no R
     assert ep(ctypes.byref(L), p, 2, p, 64, 64, big, 32, big, 64, s) == nmg.ERR_PARAM   # ldr < N
     assert ep(ctypes.byref(L), p, 2, p, 64, 64, ctypes.c_void_p((1 << 30) + 8), 64,
@@ -238,3 +238,37 @@ def test_noalloc_refuses_before_launch(lib):
               s) == nmg.ERR_UNSUPPORTED
     # the other families take nmg_spmm_epilogue's path and its checks
     assert na(ctypes.byref(L), 0, 7, p, p, p, 64, 64, None, 0, p, 64, s) == nmg.ERR_PARAM
+
+
+def test_gelu_table_rules(tmp_path):
+    """The binary16 GELU table is its own input from NMG_GELU_F16_IDENTITY_FROM
+    up (+inf included), -0 for finite negative inputs from
+    NMG_GELU_F16_NEGZERO_FROM, NMG_GELU_F16_NAN_OUT for NaN and -inf: the rules
+    the 16 x 16 x 32 product's fused GELU applies instead of those entries."""
+    import re
+    import subprocess
+    import sys
+
+    import numpy as np
+    from paper_2304_07613_amd import build
+    out = tmp_path / "gelu_f16_table.inc"
+    subprocess.run([sys.executable, build.GENERATORS[0], str(out)], check=True)
+    t = np.array([int(v, 16) for v in re.findall(r"0x([0-9a-f]{4})", out.read_text())],
+                 dtype=np.uint16)
+    assert t.size == 65536
+    bounds = dict(re.findall(r"#define (\w+) (0x[0-9a-f]+)", (tmp_path / "gelu_f16_bounds.inc").read_text()))
+    ident = int(bounds["NMG_GELU_F16_IDENTITY_FROM"], 16)
+    negz = int(bounds["NMG_GELU_F16_NEGZERO_FROM"], 16)
+    nan_out = int(bounds["NMG_GELU_F16_NAN_OUT"], 16)
+    b = np.arange(65536, dtype=np.uint32)
+    rule_pos = (b < 0x8000) & (b >= ident)
+    rule_neg = (b >= 0x8000) & (b >= negz)
+    assert (t[rule_pos & (b <= 0x7c00)] == b[rule_pos & (b <= 0x7c00)]).all()
+    assert (t[rule_pos & (b > 0x7c00)] == nan_out).all()
+    assert (t[rule_neg & (b < 0xfc00)] == 0x8000).all()
+    assert (t[rule_neg & (b >= 0xfc00)] == nan_out).all()
+    # the rules cover what they should: GELU(x) = x from about 3.45, -0 below
+    # about -5.72, and the entries kept are under 36 KB on each side
+    x = b.astype(np.uint16).view(np.float16)
+    assert 3.0 < float(x[ident]) < 4.0 and -6.0 < float(x[negz]) < -5.0
+    assert 2 * ident <= 36 * 1024 and 2 * (negz - 0x8000) <= 36 * 1024

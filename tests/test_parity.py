@@ -355,9 +355,46 @@ def test_spmm_epilogue_equals_composition(nmg, M, K, N, n, m, g, dtype):
     Yb.zero_()
     Ys = nmg.spmm_x16_epilogue(L, prepared, X, "add", Rb[:, :N], Y=Yb[:, :N])
     torch.cuda.synchronize()
-    assert torch.equal(Ys.view(torch.uint8),
-                       nmg.add(nmg.spmm(v, idx, X, L, x16), R).view(torch.uint8))
+    P = nmg.spmm(v, idx, X, L, x16)
+    assert torch.equal(Ys.view(torch.uint8), nmg.add(P, R).view(torch.uint8))
     assert (Yb[:, N:] == 0).all()
+    Yb.zero_()
+    Ys = nmg.spmm_x16_epilogue(L, prepared, X, "gelu", Y=Yb[:, :N])
+    torch.cuda.synchronize()
+    assert torch.equal(Ys.view(torch.uint8), nmg.gelu(P).view(torch.uint8))
+    assert (Yb[:, N:] == 0).all()
+
+
+def test_x16_gelu_every_input(nmg):
+    """GELU folded into the 16 x 16 x 32 product against the product followed
+    by nmg_gelu, on a product that reproduces every binary16 bit pattern
+    (except -0): each 8-row group keeps weight 1 at one X row of its own that
+    holds 256 of the patterns, every other kept weight is 0 on finite X."""
+    C, N, groups = 43, 256, 256
+    M, K = 8 * groups, 8 * C
+    W = torch.zeros((M, K), dtype=torch.float16)
+    sel = []
+    for G in range(groups):
+        col = 8 * (G % C) + 2 + G // C     # offsets 2..7: no other group keeps it
+        W[8 * G:8 * G + 8, col] = 1.0
+        sel.append(col)
+    X = synth.normal((K, N), 808, 1.0, torch.float16)
+    patt = torch.arange(65536, dtype=torch.int32).to(torch.int16).view(torch.float16)
+    for G, col in enumerate(sel):
+        X[col] = patt[G * N:(G + 1) * N]
+    v, idx, L = nmg.compress(W.to(DEV), 2, 8, 8)
+    Xd = X.to(DEV)
+    prepared = nmg.x16_prepare(v, idx, L)
+    P = nmg.spmm_x16_epilogue(L, prepared, Xd)
+    Yg = nmg.spmm_x16_epilogue(L, prepared, Xd, "gelu")
+    torch.cuda.synchronize()
+    Pb = np_of(P).view(np.uint16)
+    want = np_of(X).view(np.uint16)[sel].repeat(8, axis=0)
+    want = np.where(want == 0x8000, 0, want)       # -0 + (+0 products) = +0
+    nan = (want & 0x7c00) == 0x7c00
+    nan &= (want & 0x03ff) != 0
+    assert np.array_equal(Pb[~nan], want[~nan]) and ((Pb[nan] & 0x7c00) == 0x7c00).all()
+    assert torch.equal(Yg.view(torch.uint8), nmg.gelu(P).view(torch.uint8))
 
 
 def test_stack_fused_equals_stepwise(nmg):
