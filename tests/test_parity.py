@@ -225,6 +225,64 @@ def test_random_layouts(nmg, M, K, N, n, m, g, dtype):
         spmm_full(nmg, v, idx, L, X, rv, ridx, kernel, "random")
 
 
+def random_x16(count=40, seed=2308):
+    """Seeded random layouts the 16 x 16 x 32 products take (n of 1 or 2, g a
+    multiple of 8, binary16 m % 4 == 0 up to 12, binary32 m up to 4 / 8),
+    ragged tail chunks, rows and token tiles, with weight and X scales spread
+    over six decades (binary32: the split products' per-unit weight scaling;
+    X kept at |x| >= 1e-3 standard deviation, where their error bound is well
+    inside 1e-5 B)."""
+    rng = np.random.RandomState(seed)
+    out = []
+    while len(out) < count:
+        dtype = torch.float16 if rng.rand() < 0.5 else torch.float32
+        n = int(rng.choice([1, 2]))
+        if dtype == torch.float16:
+            m = 4 if n == 1 else int(rng.choice([4, 8, 12]))
+        else:
+            m = int(rng.randint(n, (4 if n == 1 else 8) + 1))
+        g = int(rng.choice([8, 8, 16, 24, 32, 64]))
+        C = int(rng.randint(1, 60))
+        r = m if rng.rand() < 0.5 else int(rng.randint(n, m + 1))
+        K = (C - 1) * m + r
+        M = g * int(rng.randint(1, max(2, 1024 // g)))
+        N = (8 if dtype == torch.float16 else 4) * int(rng.randint(1, 80))
+        wscale = 10.0 ** rng.uniform(-3, 3) if dtype == torch.float32 else 1.0
+        xscale = 10.0 ** rng.uniform(-3, 3) if dtype == torch.float32 else 10.0 ** rng.uniform(-2, 1)
+        if M * C * n * N > 30_000_000:
+            continue
+        out.append((M, K, N, n, m, g, dtype, wscale, xscale))
+    return out
+
+
+X16_RANDOM = random_x16()
+
+
+@pytest.mark.parametrize("M,K,N,n,m,g,dtype,wscale,xscale", X16_RANDOM,
+                         ids=[f"x{i}-{c[0]}x{c[1]}x{c[2]}-{c[3]}:{c[4]}:{c[5]}-{str(c[6])[6:]}"
+                              for i, c in enumerate(X16_RANDOM)])
+def test_x16_random(nmg, M, K, N, n, m, g, dtype, wscale, xscale):
+    """The 16 x 16 x 32 product on operands prepared once, against the
+    oracle in full (binary16: the contract and the tight bound; binary32
+    through binary16 parts: 1e-5 B), and the per-call path bit for bit."""
+    W = synth.normal((M, K), 41 + M + 5 * K, 0.02 * wscale, dtype)
+    X = synth.normal((K, N), 42 + N + 3 * K, xscale, dtype)
+    if dtype == torch.float32 and M >= 16:
+        W[:8] *= 1e-20      # a unit of tiny weights and one of large ones:
+        W[8:16] *= 1e20     # the per-unit scaling keeps both exact enough
+    v, idx, L, rv, ridx = check_compress(nmg, W, n, m, g, "x16")
+    kernel = "mfma_wide" if dtype == torch.float16 else "mfma_split"
+    print(f"[x16] {L} N={N} wscale={wscale:.3g} xscale={xscale:.3g}", flush=True)
+    prepared = nmg.x16_prepare(v, idx, L)
+    Xd = X.to(DEV)
+    Y = nmg.spmm_x16_epilogue(L, prepared, Xd)
+    Y2 = nmg.spmm(v, idx, Xd, L, kernel)
+    torch.cuda.synchronize()
+    assert torch.equal(Y.view(torch.uint8), Y2.view(torch.uint8))
+    Yref, B = oracle.spmm(rv, ridx, np_of(X), K, n, m, g)
+    check_product(Y, Yref, B, dtype, f"x16 {kernel}", L.C * L.n)
+
+
 def random_large(count=12, seed=2306):
     """Seeded random layouts at the workloads' scale (the launch shapes small
     cases never reach: 4 tokens per lane, several rounds of workgroups,
