@@ -227,7 +227,7 @@ def time_layer(ctx, args, workload, layer_no, lin, kernel_req):
     return res
 
 
-def family_times(ctx, L, sets, kernel, reps=20):
+def family_times(ctx, L, sets, kernel, reps=50):
     """Mean spmm time of each kernel family on the same rotated sets (outside
     the timed region): the evidence behind the automatic choice."""
     torch, nmg = ctx.torch, ctx.nmg
