@@ -36,16 +36,21 @@
  * CONVENTIONS FOR EVERY CALL
  *   - All data pointers are device pointers (HIP global memory) of the current
  *     device.  The caller allocates and owns every buffer; the library keeps
- *     no pointer after a call returns and allocates no device memory.
+ *     no pointer after a call returns.  The only device memory it allocates
+ *     is the scratch memory of three product families (NMG_KERNEL_MFMA_WIDE /
+ *     _SPLIT and NMG_KERNEL_MFMA_EXPAND, the last also an NMG_KERNEL_AUTO
+ *     choice), allocated and freed in stream order on the call's stream;
+ *     nmg_spmm_epilogue_noalloc uses a fixed per-GPU array instead.
  *   - Work is enqueued on `stream` (0 = the null stream) and runs
  *     asynchronously; a call returns after validation and launch.  Calls are
- *     thread-safe.  The only mutable global state is two host-side caches of
- *     HIP runtime queries that pick launch shapes: the compute-unit count per
- *     device and the resident-workgroup count per (device, kernel, workgroup
- *     size).  Each entry is filled on first use under a lock and never
- *     changes afterwards, so a call's launch shape -- and with it the order
- *     of its sums and its output bits -- depends only on its arguments and
- *     the device, whichever thread makes it.
+ *     thread-safe (nmg_spmm_epilogue_noalloc: see there).  The only mutable
+ *     global state is host-side tables filled once and never changed: the
+ *     compute-unit count per device and the resident-workgroup count per
+ *     (device, kernel, workgroup size), which pick launch shapes, and the
+ *     address of each device's fixed scratch array.  Each entry is filled on
+ *     first use under a lock, so a call's launch shape -- and with it the
+ *     order of its sums and its output bits -- depends only on its arguments
+ *     and the device, whichever thread makes it.
  *   - Launch failures are read with hipGetLastError right after the launch;
  *     an error that earlier runtime calls left pending on the calling thread
  *     is cleared first (and not reported by this library).
@@ -126,9 +131,9 @@ typedef enum nmg_kernel {
                                     ldx on 16-byte boundaries, N % 8 == 0     */
     NMG_KERNEL_VALU_STAGED = 8,  /* vector-ALU FMA on X windows staged in LDS
                                     (the choice for binary32 layouts the
-                                    matrix-core kernels decline, g = 1 above
-                                    all); needs binary32, m <= 32, n <= 16, X
-                                    and ldx on 16-byte boundaries, N % 4 == 0 */
+                                    grouped matrix-core kernels decline when m
+                                    > 8 n); needs binary32, m <= 32, n <= 16,
+                                    X and ldx on 16-byte boundaries, N % 4 == 0 */
     NMG_KERNEL_MFMA_WIDE = 9,    /* binary16 layouts on the 16 x 16 x 32
                                     binary16 matrix instruction (32 gathered
                                     k-slots of a group per instruction, binary32
