@@ -706,7 +706,8 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
 
 namespace {
 
-// waves per workgroup (one workgroup per CU, 2 per SIMD)
+// waves per workgroup (one workgroup per CU): 8, two per SIMD; binary16 also
+// 6, for layers whose 8-wave tiles would leave CUs idle
 template <bool SPLIT> constexpr int x16_waves() { return 8; }
 
 // rows per unit of the prepared operands
@@ -714,16 +715,17 @@ inline int x16_unit_rows(const nmg_layout *L) {
     return L->dtype == NMG_F32 ? 8 : (L->g % 16 == 0 ? 16 : 8);
 }
 
-// staging items per lane (SPLIT) / copy instructions per wave (HALF) and window
-inline int x16_nstg(const nmg_layout *L) {
+// staging items per lane (SPLIT) / copy instructions per wave (HALF) and
+// window, for workgroups of `nw` waves
+inline int x16_nstg(const nmg_layout *L, int nw) {
     const bool split = L->dtype == NMG_F32;
     const int rw = (kXSlots / L->n) * L->m;
     if (split) {
-        const int lanes = 64 * x16_waves<true>();
+        const int lanes = 64 * nw;
         return (rw * (kXTok / 4) + lanes - 1) / lanes;
     }
     const int inst = rw * (kXTok / 8) / 64;
-    return (inst + x16_waves<false>() - 1) / x16_waves<false>();
+    return (inst + nw - 1) / nw;
 }
 
 }  // namespace
@@ -737,7 +739,7 @@ bool nmg_internal::x16_layout_supported(const nmg_layout *L) {
     const int rowb = split ? 512 : 256;
     if (x16_buffer_bytes(L->n, L->m, rowb) > (split ? x16_buf_cap<true>() : x16_buf_cap<false>()))
         return false;
-    if (x16_nstg(L) > 8) return false;
+    if (x16_nstg(L, x16_waves<false>()) > 8) return false;
     return (int64_t)L->M * ldv < ((int64_t)1 << 31);
 }
 
@@ -779,10 +781,9 @@ struct X16Out {
     int64_t ldr;
 };
 
-template <bool SPLIT, int NS, bool U16, int GW, int NSTG>
+template <bool SPLIT, int NS, bool U16, int GW, int NW, int NSTG>
 nmg_status launch_x16_k(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
                         int N, const X16Out &o, hipStream_t stream) {
-    constexpr int NW = x16_waves<SPLIT>();
     using G = XGeom<SPLIT, U16, GW, NW>;
     // GELU only where its table and the outputs share the staging buffers
     if (o.epi == NMG_EPILOGUE_GELU &&
@@ -806,21 +807,23 @@ nmg_status launch_x16_k(const nmg_layout *L, const void *prepared, const void *X
 // the instantiated 2, 4, 6, 8): binary16 windows of 32 m / n rows take m / n
 // jobs (m = 4 at n = 1; 4, 8, 12 at n = 2), binary32 ones 2 m / n (m = 1..4 at
 // n = 1, 2..8 at n = 2)
-template <bool SPLIT, int NS>
+// With 6-wave workgroups (binary16, 2 units a wave, m <= 8): 3 to 6 jobs.
+template <bool SPLIT, int NS, int NW>
 constexpr bool x16_nstg_used(int s) {
     if constexpr (SPLIT) return s >= 2;
+    if constexpr (NW == 6) return s == 4 || s == 6;
     return NS == 1 ? s == 4 : (s >= 2 && s <= 6);
 }
 
-template <bool SPLIT, int NS, bool U16, int GW>
+template <bool SPLIT, int NS, bool U16, int GW, int NW = x16_waves<SPLIT>()>
 nmg_status launch_x16_s(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
                         int N, const X16Out &Y, hipStream_t stream) {
-    const int s = x16_nstg(L);
+    const int s = x16_nstg(L, NW);
     const int r = s <= 2 ? 2 : s <= 4 ? 4 : s <= 6 ? 6 : 8;
-#define X16_CASE(V)                                                                        \
-    case V:                                                                                \
-        if constexpr (x16_nstg_used<SPLIT, NS>(V))                                         \
-            return launch_x16_k<SPLIT, NS, U16, GW, V>(L, prepared, X, ldx, N, Y, stream); \
+#define X16_CASE(V)                                                                            \
+    case V:                                                                                    \
+        if constexpr (x16_nstg_used<SPLIT, NS, NW>(V))                                         \
+            return launch_x16_k<SPLIT, NS, U16, GW, NW, V>(L, prepared, X, ldx, N, Y, stream); \
         break;
     switch (r) {
         X16_CASE(2)
@@ -838,35 +841,57 @@ nmg_status launch_x16_s(const nmg_layout *L, const void *prepared, const void *X
 // workgroups.  Priced as rounds of workgroups (one per CU) times the rows of
 // one plus a fixed share for staging its X; binary32 at most 2 units (its
 // registers also hold the X being split), binary16 up to 3.
+// 6-wave binary16 workgroups when the window's copies split into at most 6
+// per wave (m / n <= 4 at 2 units a wave), the candidate the cost below may
+// take for layers whose 8-wave tiles leave CUs idle
+inline bool x16_six_ok(const nmg_layout *L) {
+    const int s = x16_nstg(L, 6);
+    return L->dtype == NMG_F16 && s > 2 && s <= 6;
+}
+
+// Waves and units per wave.  More rows per workgroup share each staged X
+// window (fewer bytes through the CU's load path per instruction); fewer rows
+// give more workgroups.  Priced as rounds of workgroups (one per CU) times
+// the rows of one plus a fixed share for staging its X; binary32 at most 2
+// units (its registers also hold the X being split), binary16 up to 3.  When
+// the best 8-wave shape is one round that leaves CUs idle, 6-wave workgroups
+// of 2 units that fill the GPU in one round instead (measured: attention-out
+// and FFN down of the BERT stack 0.3 and 1.5 us faster; a layer of several
+// rounds, QKV, 3 us slower).  Returns 10 * waves + units.
 template <bool SPLIT, bool U16>
-int x16_units(const nmg_layout *L, int64_t N) {
+int x16_shape(const nmg_layout *L, int64_t N) {
     constexpr int ru = SPLIT ? 8 : (U16 ? 16 : 8);
-    const int cands[3] = {3, 2, 1};
     const int64_t cus = device_cus();
     const int64_t tt = (N + kXTok - 1) / kXTok;
-    int best = 1;
+    auto wgs_of = [&](int nw, int gw) { return (L->M + (int64_t)nw * gw * ru - 1) / ((int64_t)nw * gw * ru) * tt; };
+    int best_gw = 1;
     int64_t best_cost = -1;
-    for (int gw : cands) {
+    for (int gw = 3; gw >= 1; --gw) {
         if (SPLIT && gw > 2) continue;
         const int64_t rows = (int64_t)x16_waves<SPLIT>() * gw * ru;
-        const int64_t wgs = (L->M + rows - 1) / rows * tt;
-        const int64_t cost = (wgs + cus - 1) / cus * (rows + 64);
+        const int64_t cost = (wgs_of(8, gw) + cus - 1) / cus * (rows + 64);
         if (best_cost < 0 || cost < best_cost) {
             best_cost = cost;
-            best = gw;
+            best_gw = gw;
         }
     }
-    return best;
+    if (!SPLIT && wgs_of(8, best_gw) < cus && x16_six_ok(L) && wgs_of(6, 2) <= cus &&
+        wgs_of(6, 2) > wgs_of(8, best_gw))
+        return 62;
+    return 80 + best_gw;
 }
 
 template <bool SPLIT, int NS, bool U16>
 nmg_status launch_x16_g(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
                         int N, const X16Out &Y, hipStream_t stream) {
-    switch (x16_units<SPLIT, U16>(L, N)) {
-        case 3:
+    switch (x16_shape<SPLIT, U16>(L, N)) {
+        case 83:
             if constexpr (!SPLIT) return launch_x16_s<SPLIT, NS, U16, 3>(L, prepared, X, ldx, N, Y, stream);
             return NMG_ERR_UNSUPPORTED;
-        case 2: return launch_x16_s<SPLIT, NS, U16, 2>(L, prepared, X, ldx, N, Y, stream);
+        case 82: return launch_x16_s<SPLIT, NS, U16, 2>(L, prepared, X, ldx, N, Y, stream);
+        case 62:
+            if constexpr (!SPLIT) return launch_x16_s<SPLIT, NS, U16, 2, 6>(L, prepared, X, ldx, N, Y, stream);
+            return NMG_ERR_UNSUPPORTED;
         default: return launch_x16_s<SPLIT, NS, U16, 1>(L, prepared, X, ldx, N, Y, stream);
     }
 }
