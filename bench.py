@@ -492,10 +492,21 @@ def stack(ctx, args):
     b.record(ctx.stream)
     torch.cuda.synchronize()
     ms = a.elapsed_time(b) / reps
+    # the same forward captured in a HIP graph and replayed (no host launches)
+    graph, _ = st.capture(x)
+    graph.replay()
+    torch.cuda.synchronize()
+    a.record(ctx.stream)
+    for _ in range(reps):
+        graph.replay()
+    b.record(ctx.stream)
+    torch.cuda.synchronize()
+    ms_graph = a.elapsed_time(b) / reps
     flop = 12 * sum(l.useful_flop for l in synth.bert_stack_layers())
     print(json.dumps({"metric": "BERT-base linear stack forward, useful GFLOP/s",
                       "value": round(flop / (ms * 1e-3) / 1e9, 1), "unit": "GFLOP/s",
                       "ms_per_forward": round(ms, 4),
+                      "ms_per_forward_graph": round(ms_graph, 4),
                       "tokens_per_s": round(synth.BERT_TOKENS / (ms * 1e-3), 1),
                       "dtype": "f16 (binary32 accumulate)", "layers": 12, "reps": reps,
                       "kernels": kernels,

@@ -112,3 +112,21 @@ class LinearStack:
         for layer in self.layers:
             x = self.forward_layer(layer, x)
         return x
+
+    def capture(self, x: torch.Tensor):
+        """The forward on x captured in a HIP graph: returns (graph, y), where
+        graph.replay() recomputes y from the current contents of x with no
+        host-side launches.  Every step is a library kernel that allocates
+        nothing and writes no memory with a memset; torch's graph pool holds
+        the intermediate buffers."""
+        side = torch.cuda.Stream(device=x.device)
+        side.wait_stream(torch.cuda.current_stream(x.device))
+        with torch.cuda.stream(side):
+            for _ in range(2):   # launch shapes cached, torch's pool warmed
+                self.forward(x)
+        torch.cuda.current_stream(x.device).wait_stream(side)
+        torch.cuda.synchronize(x.device)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            y = self.forward(x)
+        return graph, y

@@ -455,6 +455,25 @@ def test_x16_gelu_every_input(nmg):
     assert torch.equal(Yg.view(torch.uint8), nmg.gelu(P).view(torch.uint8))
 
 
+def test_stack_graph_replay(nmg):
+    """Two BERT layers captured in a HIP graph: every replay, with eager work
+    and synchronisations between the replays, gives the eager forward's bits,
+    also after the input changes."""
+    from paper_2304_07613_amd.stack import LinearStack
+    stack = LinearStack.from_workload(4, nmg, n_layers=2, keep_dense=False)
+    x = synth.normal((synth.BERT_HIDDEN, synth.BERT_TOKENS), synth.seed_for(4, 0, "X"), 1.0,
+                     torch.float16).to(DEV)
+    graph, y = stack.capture(x)
+    for rep in range(4):
+        if rep == 2:   # new input, written in place
+            x.copy_(synth.normal(tuple(x.shape), 4321, 1.0, torch.float16).to(DEV))
+        eager = stack.forward(x)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y.view(torch.int16), eager.view(torch.int16)), f"replay {rep}"
+
+
 def test_stack_fused_equals_stepwise(nmg):
     """One BERT layer: the fused forward gives the bits of the step-by-step
     forward whose every step the stack test checks against the oracle."""
