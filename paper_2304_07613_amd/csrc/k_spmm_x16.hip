@@ -151,15 +151,16 @@ struct XGeom {
 // table entries that are not a rule -- non-negative inputs below
 // NMG_GELU_F16_IDENTITY_FROM in buffer 0, negative ones below
 // NMG_GELU_F16_NEGZERO_FROM in buffer 1 -- and the waves' output regions go
-// to buffer 2 and to what the tables leave of buffers 0 and 1.
+// to buffers 2 (and 3) and to what the tables leave of buffers 0 and 1.
 constexpr int kGeluPosBytes = (2 * NMG_GELU_F16_IDENTITY_FROM + 255) / 256 * 256;
 constexpr int kGeluNegBytes = (2 * (NMG_GELU_F16_NEGZERO_FROM - 0x8000) + 255) / 256 * 256;
 __host__ __device__ constexpr int x16_out_region(bool split, int rows_wave) {
     return rows_wave * (kXTok * (split ? 4 : 2) + 32);
 }
-__host__ __device__ constexpr bool x16_gelu_fits(bool split, int rows_wave, int waves, int bufcap) {
-    return !split && kGeluPosBytes <= bufcap && kGeluNegBytes <= bufcap &&
-           bufcap / x16_out_region(split, rows_wave) +
+__host__ __device__ constexpr bool x16_gelu_fits(bool split, int rows_wave, int waves, int bufcap,
+                                                 int nbuf) {
+    return !split && nbuf >= 3 && kGeluPosBytes <= bufcap && kGeluNegBytes <= bufcap &&
+           (nbuf - 2) * (bufcap / x16_out_region(split, rows_wave)) +
                    (bufcap - kGeluPosBytes) / x16_out_region(split, rows_wave) +
                    (bufcap - kGeluNegBytes) / x16_out_region(split, rows_wave) >=
                waves;
@@ -170,10 +171,14 @@ inline int x16_buffer_bytes(int n, int m, int row_bytes) {
     const int cs = m * row_bytes + 32;
     return ((kXSlots / n) * cs + 255) / 256 * 256;
 }
-// Staging buffers: binary16 three (window w + 2 is copied while w is
-// multiplied), binary32 two (its X passes through registers one window ahead)
-template <bool SPLIT> constexpr int x16_nbuf() { return SPLIT ? 2 : 3; }
-template <bool SPLIT> constexpr int x16_buf_cap() { return SPLIT ? 81920 : 53248; }
+// Staging buffers: binary16 DP + 1 when windows are copied DP ahead (four
+// of 40 KB when a window fits, copies three windows ahead; else three of 52
+// KB, two ahead), binary32 two (its X passes through registers one window
+// ahead, DP = 1)
+template <bool SPLIT, int DP> constexpr int x16_nbuf() { return SPLIT ? 2 : DP + 1; }
+template <bool SPLIT, int DP> constexpr int x16_buf_cap() {
+    return SPLIT ? 81920 : DP == 3 ? 40960 : 53248;
+}
 
 // ---------------------------------------------------------------- prepared operands
 //
@@ -282,7 +287,7 @@ __global__ __launch_bounds__(64) void k_x16_prepare(const void *__restrict__ val
 
 // R_ == nullptr: Y = P; else Y = P + R (the sum in binary32 of the product
 // rounded to the element type and R, rounded again)
-template <bool SPLIT, int NS, bool U16, int GW, int NW, int NSTG>
+template <bool SPLIT, int NS, bool U16, int GW, int NW, int NSTG, int DP>
 __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
     const h8 *__restrict__ frag, const uint16_t *__restrict__ offs, const int8_t *__restrict__ scale,
     const void *__restrict__ X_, int64_t ldx, void *__restrict__ Y_, int64_t ldy,
@@ -291,14 +296,15 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
     using G = XGeom<SPLIT, U16, GW, NW>;
     constexpr int RU = G::rows_unit, ROWB = G::row_bytes;
     constexpr int CPW = kXSlots / NS;  // chunks per window
-    constexpr int NBUF = x16_nbuf<SPLIT>();
-    constexpr int BUFCAP = x16_buf_cap<SPLIT>();
+    constexpr int NBUF = x16_nbuf<SPLIT, DP>();
+    constexpr int BUFCAP = x16_buf_cap<SPLIT, DP>();
     static_assert(NS == 1 || NS == 2, "n of 1 or 2");
     // the staging buffers as distinct objects, so that the compiler can tell
     // the copies into one from the reads of another
     __shared__ __attribute__((aligned(256))) char xs0[BUFCAP];
     __shared__ __attribute__((aligned(256))) char xs1[BUFCAP];
-    __shared__ __attribute__((aligned(256))) char xs2[NBUF == 3 ? BUFCAP : 16];
+    __shared__ __attribute__((aligned(256))) char xs2[NBUF >= 3 ? BUFCAP : 16];
+    __shared__ __attribute__((aligned(256))) char xs3[NBUF >= 4 ? BUFCAP : 16];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -500,28 +506,32 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
         });
     };
 
-    // ---- the pipeline.  HALF: operands and X copies two windows ahead
-    // (three buffers); at the end of window w the copies of w + 1 must have
-    // landed, and after them this wave issued only the operand loads of w + 2
-    // (2 GW) and the copies of w + 2 (NSTG): it waits until at most that many
-    // are outstanding.  SPLIT: operands and X one window ahead (X through
-    // registers, split and written after the products).
-    constexpr int DIST = SPLIT ? 1 : 2;     // windows ahead
+    // ---- the pipeline.  HALF: operands and X copies DP windows ahead (DP +
+    // 1 buffers); at the end of window w the copies of w + 1 must have
+    // landed, and after them this wave issued only the operand loads (2 GW)
+    // and the copies (NSTG) of windows w + 2 .. w + DP: it waits until at
+    // most that many are outstanding.  SPLIT: operands and X one window
+    // ahead (X through registers, split and written after the products).
+    constexpr int DIST = SPLIT ? 1 : DP;    // windows ahead
+    static_assert(SPLIT ? DP == 1 : (DP == 2 || DP == 3), "pipeline depth");
     constexpr int NOPS = DIST + 1;          // operand sets in rotation
-    char *const bufs[3] = {xs0, xs1, xs2};
+    char *const bufs[4] = {xs0, xs1, xs2, xs3};
     Ops ops[NOPS];
     uint32_t aa[2][GW][2];
-    load_ops(0, ops[0]);
-    if constexpr (DIST == 2) load_ops(1, ops[1]);
-    stage_issue(0, xs0);
-    if constexpr (!SPLIT) stage_issue(1, xs1);
+    static_for<DIST>([&](auto dc) { load_ops(decltype(dc)::value, ops[decltype(dc)::value]); });
+    if constexpr (SPLIT) {
+        stage_issue(0, xs0);
+    } else {
+        static_for<DIST>([&](auto dc) { stage_issue(decltype(dc)::value, bufs[decltype(dc)::value]); });
+    }
     stage_write(xs0);
     wait_all_memory();
     addresses(ops[0], aa[0]);
-    if constexpr (DIST == 2) addresses(ops[1], aa[1]);
+    if constexpr (DIST >= 2) addresses(ops[1], aa[1]);
     __syncthreads();
-    // step w (W6 = w % 6, so that operand sets, address sets and buffers
+    // step w (W6 = w % PERIOD, so that operand sets, address sets and buffers
     // rotate statically): window w from bufs[W6 % NBUF]
+    constexpr int PERIOD = NOPS == 4 ? 4 : 6;  // a multiple of NOPS, NBUF and 2
     auto step = [&](int w, auto w6c) __attribute__((always_inline)) {
         constexpr int W6 = decltype(w6c)::value;
         Ops &cur = ops[W6 % NOPS];
@@ -547,23 +557,16 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
             window_barrier<2 * GW>();  // operand loads of w + 1 may stay in flight
         } else {
             addresses(nxt, an);
-            window_barrier<2 * GW + NSTG>();
+            window_barrier<(DIST - 1) * (2 * GW + NSTG)>();
         }
     };
+    static_assert(PERIOD % NOPS == 0 && PERIOD % NBUF == 0 && PERIOD % 2 == 0, "static rotation");
     int w = 0;
-    for (; w + 6 <= nwin; w += 6) {
-        step(w + 0, std::integral_constant<int, 0>{});
-        step(w + 1, std::integral_constant<int, 1>{});
-        step(w + 2, std::integral_constant<int, 2>{});
-        step(w + 3, std::integral_constant<int, 3>{});
-        step(w + 4, std::integral_constant<int, 4>{});
-        step(w + 5, std::integral_constant<int, 5>{});
-    }
-    if (w < nwin) step(w, std::integral_constant<int, 0>{});
-    if (w + 1 < nwin) step(w + 1, std::integral_constant<int, 1>{});
-    if (w + 2 < nwin) step(w + 2, std::integral_constant<int, 2>{});
-    if (w + 3 < nwin) step(w + 3, std::integral_constant<int, 3>{});
-    if (w + 4 < nwin) step(w + 4, std::integral_constant<int, 4>{});
+    for (; w + PERIOD <= nwin; w += PERIOD)
+        static_for<PERIOD>([&](auto kc) { step(w + decltype(kc)::value, kc); });
+    static_for<PERIOD - 1>([&](auto kc) {
+        if (w + decltype(kc)::value < nwin) step(w + decltype(kc)::value, kc);
+    });
 
     // ---- the outputs, through LDS: each wave writes its rows x 128 tokens
     // into a region of its own (rows padded by 32 bytes, so that the 8 rows a
@@ -576,7 +579,7 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
     static_assert(RB == x16_out_region(SPLIT, G::rows_wave), "one region formula");
     constexpr int WPA = BUFCAP / RB;                 // regions per staging buffer
     static_assert(WPA >= 1 && WPA * NBUF >= NW, "output regions fit the staging buffers");
-    constexpr bool GELU_OK = NBUF == 3 && x16_gelu_fits(SPLIT, G::rows_wave, NW, BUFCAP);
+    constexpr bool GELU_OK = x16_gelu_fits(SPLIT, G::rows_wave, NW, BUFCAP, NBUF);
     const bool gelu = GELU_OK && epi == NMG_EPILOGUE_GELU;  // the host asks only when it fits
     // the GELU table's non-rule entries, 16 bytes a thread and step, all loads
     // in flight together before the barrier (the buffers are free after it)
@@ -597,7 +600,8 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
     }
     window_barrier<0>();  // copies for windows past the last have landed; every wave is done
     const int oreg = wave / WPA;
-    lds_char *ob = (lds_char *)(oreg == 0 ? xs0 : (NBUF == 2 || oreg == 1) ? xs1 : xs2) + (wave % WPA) * RB;
+    lds_char *ob = (lds_char *)(oreg == 0 ? xs0 : (NBUF == 2 || oreg == 1) ? xs1 : (NBUF == 3 || oreg == 2) ? xs2 : xs3) +
+                   (wave % WPA) * RB;
     if constexpr (GELU_OK) {
         if (gelu) {
             // into buffers 0 (non-negative inputs) and 1 (negative ones)
@@ -611,10 +615,12 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
                 if ((int)threadIdx.x + j * TPB < NTN)
                     ((lds_f4 *)(lds_char *)xs1)[threadIdx.x + j * TPB] = tabn[j];
             window_barrier<0>();  // every wave's table writes are done
-            constexpr int W2 = BUFCAP / RB, W0 = (BUFCAP - kGeluPosBytes) / RB;
+            constexpr int W2 = BUFCAP / RB, W3 = NBUF >= 4 ? BUFCAP / RB : 0;
+            constexpr int W0 = (BUFCAP - kGeluPosBytes) / RB;
             ob = wave < W2 ? (lds_char *)xs2 + wave * RB
-                 : wave < W2 + W0 ? (lds_char *)xs0 + kGeluPosBytes + (wave - W2) * RB
-                                  : (lds_char *)xs1 + kGeluNegBytes + (wave - W2 - W0) * RB;
+                 : wave < W2 + W3 ? (lds_char *)xs3 + (wave - W2) * RB
+                 : wave < W2 + W3 + W0 ? (lds_char *)xs0 + kGeluPosBytes + (wave - W2 - W3) * RB
+                                       : (lds_char *)xs1 + kGeluNegBytes + (wave - W2 - W3 - W0) * RB;
         }
     }
 #pragma unroll
@@ -737,7 +743,7 @@ bool nmg_internal::x16_layout_supported(const nmg_layout *L) {
     if (L->g % 8 != 0) return false;
     if (!split && L->m % 4 != 0) return false;          // whole-wave LDS copies of 4 rows
     const int rowb = split ? 512 : 256;
-    if (x16_buffer_bytes(L->n, L->m, rowb) > (split ? x16_buf_cap<true>() : x16_buf_cap<false>()))
+    if (x16_buffer_bytes(L->n, L->m, rowb) > (split ? x16_buf_cap<true, 1>() : x16_buf_cap<false, 2>()))
         return false;
     if (x16_nstg(L, x16_waves<false>()) > 8) return false;
     return (int64_t)L->M * ldv < ((int64_t)1 << 31);
@@ -781,13 +787,13 @@ struct X16Out {
     int64_t ldr;
 };
 
-template <bool SPLIT, int NS, bool U16, int GW, int NW, int NSTG>
+template <bool SPLIT, int NS, bool U16, int GW, int NW, int NSTG, int DP>
 nmg_status launch_x16_k(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
                         int N, const X16Out &o, hipStream_t stream) {
     using G = XGeom<SPLIT, U16, GW, NW>;
     // GELU only where its table and the outputs share the staging buffers
     if (o.epi == NMG_EPILOGUE_GELU &&
-        !(x16_nbuf<SPLIT>() == 3 && x16_gelu_fits(SPLIT, G::rows_wave, NW, x16_buf_cap<SPLIT>())))
+        !x16_gelu_fits(SPLIT, G::rows_wave, NW, x16_buf_cap<SPLIT, DP>(), x16_nbuf<SPLIT, DP>()))
         return NMG_ERR_UNSUPPORTED;
     const XPrep P = x16_prep_layout(L, G::rows_unit);
     const char *base = static_cast<const char *>(prepared);
@@ -796,7 +802,7 @@ nmg_status launch_x16_k(const nmg_layout *L, const void *prepared, const void *X
     const h8 *fr = reinterpret_cast<const h8 *>(base + P.frag);
     const uint16_t *of = reinterpret_cast<const uint16_t *>(base + P.offs);
     const int8_t *sc = reinterpret_cast<const int8_t *>(base + P.scale);
-    hipLaunchKernelGGL((k_spmm_x16<SPLIT, NS, U16, GW, NW, NSTG>), dim3(grid), dim3(64 * NW), 0,
+    hipLaunchKernelGGL((k_spmm_x16<SPLIT, NS, U16, GW, NW, NSTG, DP>), dim3(grid), dim3(64 * NW), 0,
                        stream, fr, of, sc, X, ldx, o.Y, o.ldy,
                        o.epi == NMG_EPILOGUE_ADD ? o.R : nullptr, o.ldr, o.epi, L->M, L->K, N,
                        L->m, P.nwin, row_blocks);
@@ -815,15 +821,32 @@ constexpr bool x16_nstg_used(int s) {
     return NS == 1 ? s == 4 : (s >= 2 && s <= 6);
 }
 
+// The pipeline depth of each instantiation: binary16 6-wave workgroups (the
+// single-round layers, whose windows all fit 40 KB) copy three windows
+// ahead, 8-wave ones two; binary32 one.  Measured on the BERT stack: FFN
+// down (24 windows, 6-wave) 22.6 -> 20.6 us at depth 3; at depth 3 the
+// 8-wave layers of 6 windows were 0.7 us slower (QKV, FFN up).
+template <bool SPLIT, int NS, int NW, int NSTG>
+constexpr int x16_dp_of() {
+    if constexpr (SPLIT) return 1;
+    return NW == 6 ? 3 : 2;
+}
+
 template <bool SPLIT, int NS, bool U16, int GW, int NW = x16_waves<SPLIT>()>
 nmg_status launch_x16_s(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
                         int N, const X16Out &Y, hipStream_t stream) {
     const int s = x16_nstg(L, NW);
     const int r = s <= 2 ? 2 : s <= 4 ? 4 : s <= 6 ? 6 : 8;
-#define X16_CASE(V)                                                                            \
-    case V:                                                                                    \
-        if constexpr (x16_nstg_used<SPLIT, NS, NW>(V))                                         \
-            return launch_x16_k<SPLIT, NS, U16, GW, NW, V>(L, prepared, X, ldx, N, Y, stream); \
+    // a window must fit the buffers of the instantiation's depth
+    const int wbytes = x16_buffer_bytes(L->n, L->m, SPLIT ? 512 : 256);
+#define X16_CASE(V)                                                                                \
+    case V:                                                                                        \
+        if constexpr (x16_nstg_used<SPLIT, NS, NW>(V)) {                                           \
+            constexpr int DPV = x16_dp_of<SPLIT, NS, NW, V>();                                     \
+            if (wbytes <= x16_buf_cap<SPLIT, DPV>())                                               \
+                return launch_x16_k<SPLIT, NS, U16, GW, NW, V, DPV>(L, prepared, X, ldx, N, Y,     \
+                                                                    stream);                       \
+        }                                                                                          \
         break;
     switch (r) {
         X16_CASE(2)
