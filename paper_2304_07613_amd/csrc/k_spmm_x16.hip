@@ -876,32 +876,30 @@ inline bool x16_six_ok(const nmg_layout *L) {
 // window (fewer bytes through the CU's load path per instruction); fewer rows
 // give more workgroups.  Priced as rounds of workgroups (one per CU) times
 // the rows of one plus a fixed share for staging its X; binary32 at most 2
-// units (its registers also hold the X being split), binary16 up to 3.  When
-// the best 8-wave shape is one round that leaves CUs idle, 6-wave workgroups
-// of 2 units that fill the GPU in one round instead (measured: attention-out
-// and FFN down of the BERT stack 0.3 and 1.5 us faster; a layer of several
-// rounds, QKV, 3 us slower).  Returns 10 * waves + units.
+// units (its registers also hold the X being split), binary16 up to 3, also
+// in 6-wave workgroups (2 or 3 units) when the window's copies split into at
+// most 6 per wave.  Returns 10 * waves + units.
 template <bool SPLIT, bool U16>
 int x16_shape(const nmg_layout *L, int64_t N) {
     constexpr int ru = SPLIT ? 8 : (U16 ? 16 : 8);
+    const int cands[5][2] = {{8, 3}, {8, 2}, {8, 1}, {6, 3}, {6, 2}};
     const int64_t cus = device_cus();
     const int64_t tt = (N + kXTok - 1) / kXTok;
-    auto wgs_of = [&](int nw, int gw) { return (L->M + (int64_t)nw * gw * ru - 1) / ((int64_t)nw * gw * ru) * tt; };
-    int best_gw = 1;
+    int best = 81;
     int64_t best_cost = -1;
-    for (int gw = 3; gw >= 1; --gw) {
-        if (SPLIT && gw > 2) continue;
-        const int64_t rows = (int64_t)x16_waves<SPLIT>() * gw * ru;
-        const int64_t cost = (wgs_of(8, gw) + cus - 1) / cus * (rows + 64);
+    for (const auto &c : cands) {
+        const int nw = c[0], gw = c[1];
+        if (SPLIT && (gw > 2 || nw != 8)) continue;
+        if (nw == 6 && !x16_six_ok(L)) continue;
+        const int64_t rows = (int64_t)nw * gw * ru;
+        const int64_t wgs = (L->M + rows - 1) / rows * tt;
+        const int64_t cost = (wgs + cus - 1) / cus * (rows + 64);
         if (best_cost < 0 || cost < best_cost) {
             best_cost = cost;
-            best_gw = gw;
+            best = 10 * nw + gw;
         }
     }
-    if (!SPLIT && wgs_of(8, best_gw) < cus && x16_six_ok(L) && wgs_of(6, 2) <= cus &&
-        wgs_of(6, 2) > wgs_of(8, best_gw))
-        return 62;
-    return 80 + best_gw;
+    return best;
 }
 
 template <bool SPLIT, int NS, bool U16>
@@ -912,6 +910,9 @@ nmg_status launch_x16_g(const nmg_layout *L, const void *prepared, const void *X
             if constexpr (!SPLIT) return launch_x16_s<SPLIT, NS, U16, 3>(L, prepared, X, ldx, N, Y, stream);
             return NMG_ERR_UNSUPPORTED;
         case 82: return launch_x16_s<SPLIT, NS, U16, 2>(L, prepared, X, ldx, N, Y, stream);
+        case 63:
+            if constexpr (!SPLIT) return launch_x16_s<SPLIT, NS, U16, 3, 6>(L, prepared, X, ldx, N, Y, stream);
+            return NMG_ERR_UNSUPPORTED;
         case 62:
             if constexpr (!SPLIT) return launch_x16_s<SPLIT, NS, U16, 2, 6>(L, prepared, X, ldx, N, Y, stream);
             return NMG_ERR_UNSUPPORTED;
