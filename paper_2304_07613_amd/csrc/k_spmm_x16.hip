@@ -113,6 +113,15 @@ __device__ __forceinline__ void window_barrier() {
 #endif
 }
 
+// All LDS operations of this wave done, then the workgroup barrier (memory
+// operations, LDS copies included, may stay in flight)
+__device__ __forceinline__ void lds_barrier() {
+#if defined(__HIP_DEVICE_COMPILE__)
+    __builtin_amdgcn_s_waitcnt(waitcnt_imm(63, true));
+    asm volatile("s_barrier" ::: "memory");
+#endif
+}
+
 // a + (the value of lane l ^ 8 of the same 16-lane row)
 __device__ __forceinline__ float add_row_ror8(float a) {
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -287,7 +296,7 @@ __global__ __launch_bounds__(64) void k_x16_prepare(const void *__restrict__ val
 
 // R_ == nullptr: Y = P; else Y = P + R (the sum in binary32 of the product
 // rounded to the element type and R, rounded again)
-template <bool SPLIT, int NS, bool U16, int GW, int NW, int NSTG, int DP>
+template <bool SPLIT, int NS, bool U16, int GW, int NW, int NSTG, int DP, int TPW>
 __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
     const h8 *__restrict__ frag, const uint16_t *__restrict__ offs, const int8_t *__restrict__ scale,
     const void *__restrict__ X_, int64_t ldx, void *__restrict__ Y_, int64_t ldy,
@@ -299,6 +308,7 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
     constexpr int NBUF = x16_nbuf<SPLIT, DP>();
     constexpr int BUFCAP = x16_buf_cap<SPLIT, DP>();
     static_assert(NS == 1 || NS == 2, "n of 1 or 2");
+    static_assert(TPW == 1 || (TPW == 2 && !SPLIT && DP == 2), "two tiles: binary16, two windows ahead");
     // the staging buffers as distinct objects, so that the compiler can tell
     // the copies into one from the reads of another
     __shared__ __attribute__((aligned(256))) char xs0[BUFCAP];
@@ -313,11 +323,14 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
     const int rw = CPW * m;         // X rows per window
     const int units = M / RU;
 
-    // this workgroup's tile: row block rb, 128 tokens from t0 (tiles of one
-    // token range are adjacent, so an XCD's workgroups share X in its L2)
+    // this workgroup's tiles: row block rb, TPW tiles of 128 tokens from t0
+    // (tiles of one token range are adjacent, so an XCD's workgroups share X
+    // in its L2); its steps are the windows of its tiles, one after the other
     const int tile = xcd_tile(blockIdx.x, gridDim.x);
     const int rb = tile % row_blocks;
-    const int t0 = (tile / row_blocks) * kXTok;
+    const int t0 = (tile / row_blocks) * (TPW * kXTok);
+    const int ntile = TPW == 1 ? 1 : min(TPW, (N - t0 + kXTok - 1) / kXTok);
+    const int nstep = ntile * nwin;
     const int row_w = rb * G::rows_wg + wave * G::rows_wave;  // first row of this wave
     int ug[GW];                                               // this wave's units (clamped)
 #pragma unroll
@@ -364,7 +377,9 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
     // item k of window w's staging
     auto stage_one = [&](int w, char *buf, auto kc) __attribute__((always_inline)) {
         constexpr int k = decltype(kc)::value;
-        const int k0 = w * rw;
+        // step w: window w % nwin of tile w / nwin
+        const int tj = (TPW > 1 && w >= nwin) ? 1 : 0;
+        const int k0 = (w - tj * nwin) * rw;
         if constexpr (SPLIT) {
             const int row = min(st_row0 + k * SROWS, rw - 1);
             const int xr = min(k0 + row, K - 1);           // rows past K: never selected
@@ -374,7 +389,7 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
             const int row0 = 4 * j;                         // first row of the four, in the window
             const int c = div_m(row0), o = row0 - c * m;    // its chunk and offset (uniform)
             const int xr = min(k0 + row0 + cp_sub, K - 1);
-            const int tok = min(t0 + cp_tok, N - 8);
+            const int tok = min(t0 + tj * kXTok + cp_tok, N - 8);
             lds_copy16(Xh + (int64_t)xr * ldx + tok, reinterpret_cast<_Float16 *>(buf + c * cs + o * ROWB));
         }
     };
@@ -418,7 +433,8 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
     const int flane = (!SPLIT && !U16) ? (lane & ~8) : lane;
     auto load_one = [&](int w, Ops &op, auto uc) __attribute__((always_inline)) {
         constexpr int u = decltype(uc)::value;
-        const size_t e = ((size_t)ug[u] * nwin + min(w, nwin - 1)) * 64;
+        const int wc = min(w, nstep - 1);
+        const size_t e = ((size_t)ug[u] * nwin + ((TPW > 1 && wc >= nwin) ? wc - nwin : wc)) * 64;
         op.b[u] = frag[e + flane];
         op.o[u] = offs[e + lane];
     };
@@ -506,6 +522,108 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
         });
     };
 
+    // ---- the outputs go through LDS: each wave writes its rows x 128 tokens
+    // into a region of its own (rows padded by 32 bytes, so that the 8 rows a
+    // write instruction touches fall on distinct banks; by 16 where a tile's
+    // outputs must fit the one buffer free in the middle of the pipeline),
+    // then stores whole rows, 16 bytes per lane (a full 256- or 512-byte run
+    // per row, instead of 32- or 64-byte pieces from the instruction's own
+    // layout)
+    constexpr int ES = SPLIT ? 4 : 2;
+    constexpr int RSTRIDE = kXTok * ES + ((TPW > 1 && NW * G::rows_wave * (kXTok * ES + 32) > BUFCAP) ? 16 : 32);
+    constexpr int RB = G::rows_wave * RSTRIDE;       // one wave's region
+    static_assert(TPW > 1 || RB == x16_out_region(SPLIT, G::rows_wave), "one region formula");
+    static_assert(TPW == 1 || NW * RB <= BUFCAP, "a tile's outputs fit one staging buffer");
+    constexpr int LPR = kXTok * ES / 16;              // lanes per row
+    constexpr int RPI = 64 / LPR;                     // rows per instruction
+    constexpr int NST = G::rows_wave / RPI;           // store instructions per wave and tile
+    bool after_out = false;                           // the steps after a tile's outputs
+
+    // a tile's outputs: acc -> this wave's region at ob -> whole rows of Y
+    // (tokens from tb), GELU or the residual sum applied on the way
+    constexpr bool GELU_OK = TPW == 1 && x16_gelu_fits(SPLIT, G::rows_wave, NW, BUFCAP, NBUF);
+    auto tile_out = [&](lds_char *ob, int tb, bool gelu) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < GW; ++u) {
+            const float sc = SPLIT ? __builtin_ldexpf(1.f, -(int)scale[ug[u]]) : 1.f;
+#pragma unroll
+            for (int t = 0; t < kXTiles; ++t) {
+                f4 d = acc[u][t];
+                const uint32_t col = (uint32_t)((16 * t + 4 * q) * ES);
+                if constexpr (SPLIT) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) d[i] = add_row_ror8(d[i]) * sc;
+                    if (p < 8) *(__attribute__((address_space(3))) f4 *)(ob + (u * RU + p) * RSTRIDE + col) = d;
+                } else {
+                    if (U16 || p < 8)
+                        *(lds_u2 *)(ob + (u * RU + p) * RSTRIDE + col) =
+                            u32x2{pack_h2((_Float16)d[0], (_Float16)d[1]), pack_h2((_Float16)d[2], (_Float16)d[3])};
+                }
+            }
+        }
+        const int orow = lane / LPR, ocol = lane % LPR;
+        const int tok = tb + ocol * (16 / ES);
+        // a wave whose rows and tokens are all inside Y stores without a guard per
+        // row, so that the compiler may overlap the rows' LDS reads
+        const bool whole = row_w + G::rows_wave <= M && tb + kXTok <= N;
+        auto store_rows = [&](auto guarded) __attribute__((always_inline)) {
+#pragma unroll
+        for (int r0 = 0; r0 < G::rows_wave; r0 += RPI) {
+            const int r = r0 + orow;
+            f4 v = *(__attribute__((address_space(3))) f4 *)(ob + r * RSTRIDE + ocol * 16);
+            const int row = row_w + r;
+            if (!decltype(guarded)::value || (row < M && tok < N)) {
+                if constexpr (GELU_OK) {
+                    if (gelu) {
+                        typedef __attribute__((address_space(3))) const uint16_t lds_u16;
+                        typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+                        const u32x4 a = __builtin_bit_cast(u32x4, v);  // 8 binary16, two per word
+                        u32x4 o = {0u, 0u, 0u, 0u};
+                        lds_u16 *const tab0 = (lds_u16 *)(lds_char *)xs0;
+                        lds_u16 *const tab1 = (lds_u16 *)(lds_char *)xs1;
+                        // branch-free: one LDS read per element, at an in-bounds
+                        // entry of the sign's table (all 8 issued before any is
+                        // used), then the rule where the table has no entry
+                        uint32_t bb[8], lim[8], tv[8];
+#pragma unroll
+                        for (int i = 0; i < 8; ++i) {
+                            bb[i] = (a[i >> 1] >> (16 * (i & 1))) & 0xffffu;
+                            lim[i] = (bb[i] >> 15) ? (uint32_t)(NMG_GELU_F16_NEGZERO_FROM - 0x8001)
+                                                   : (uint32_t)(NMG_GELU_F16_IDENTITY_FROM - 1);
+                            tv[i] = ((bb[i] >> 15) ? tab1 : tab0)[min(bb[i] & 0x7fffu, lim[i])];
+                        }
+#pragma unroll
+                        for (int i = 0; i < 8; ++i) {
+                            const uint32_t b = bb[i];
+                            const uint32_t rule = b <= 0x7c00u ? b
+                                                  : (b - 0x8000u) < 0x7c00u ? 0x8000u
+                                                                           : (uint32_t)NMG_GELU_F16_NAN_OUT;
+                            o[i >> 1] |= ((b & 0x7fffu) <= lim[i] ? tv[i] : rule) << (16 * (i & 1));
+                        }
+                        v = __builtin_bit_cast(f4, o);
+                    }
+                }
+                if (R_ != nullptr) {
+                    const f4 rv = *reinterpret_cast<const f4 *>(reinterpret_cast<const char *>(R_) +
+                                                                ((int64_t)row * ldr + tok) * ES);
+                    if constexpr (SPLIT) {
+                        v = v + rv;
+                    } else {
+                        const h8 a = __builtin_bit_cast(h8, v), b = __builtin_bit_cast(h8, rv);
+                        h8 o;
+#pragma unroll
+                        for (int i = 0; i < 8; ++i) o[i] = (_Float16)((float)a[i] + (float)b[i]);
+                        v = __builtin_bit_cast(f4, o);
+                    }
+                }
+                store_y(v, reinterpret_cast<f4 *>(reinterpret_cast<char *>(Y_) + ((int64_t)row * ldy + tok) * ES));
+            }
+        }
+        };
+        if (whole) store_rows(std::false_type{});
+        else store_rows(std::true_type{});
+    };
+
     // ---- the pipeline.  HALF: operands and X copies DP windows ahead (DP +
     // 1 buffers); at the end of window w the copies of w + 1 must have
     // landed, and after them this wave issued only the operand loads (2 GW)
@@ -543,7 +661,7 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
         // operands (so that at the window's end the copies of w + 1 are
         // followed by exactly the window's own 2 GW + NSTG loads or more)
         char *sbuf = bufs[(W6 + DIST) % NBUF];
-        const int ws = min(w + DIST, nwin - 1);
+        const int ws = min(w + DIST, nstep - 1);
         compute(
             bufs[W6 % NBUF], cur, ac,
             [&](auto jc) __attribute__((always_inline)) {
@@ -557,29 +675,48 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
             window_barrier<2 * GW>();  // operand loads of w + 1 may stay in flight
         } else {
             addresses(nxt, an);
-            window_barrier<(DIST - 1) * (2 * GW + NSTG)>();
+            if constexpr (TPW > 1 && W6 < DIST - 1) {
+                // the first steps after a tile's outputs: its NST stores,
+                // issued after the copies of window w + 1, may stay in flight
+                if (after_out) window_barrier<(DIST - 1) * (2 * GW + NSTG) + NST>();
+                else window_barrier<(DIST - 1) * (2 * GW + NSTG)>();
+            } else {
+                window_barrier<(DIST - 1) * (2 * GW + NSTG)>();
+            }
         }
     };
     static_assert(PERIOD % NOPS == 0 && PERIOD % NBUF == 0 && PERIOD % 2 == 0, "static rotation");
-    int w = 0;
-    for (; w + PERIOD <= nwin; w += PERIOD)
-        static_for<PERIOD>([&](auto kc) { step(w + decltype(kc)::value, kc); });
-    static_for<PERIOD - 1>([&](auto kc) {
-        if (w + decltype(kc)::value < nwin) step(w + decltype(kc)::value, kc);
-    });
+    if constexpr (TPW > 1) {
+        // nwin % PERIOD == 0 (host): every tile ends a block of PERIOD steps
+        for (int w = 0; w < nstep; w += PERIOD) {
+            static_for<PERIOD>([&](auto kc) { step(w + decltype(kc)::value, kc); });
+            after_out = false;
+            if (w + PERIOD < nstep && (w + PERIOD) % nwin == 0) {
+                // a tile's outputs through the buffer of its last window (the
+                // step's barrier: every wave is done with it) while the next
+                // tile's first windows are in flight into the other buffers
+                tile_out((lds_char *)bufs[(PERIOD - 1) % NBUF] + wave * RB,
+                         t0 + ((w + PERIOD) / nwin - 1) * kXTok, false);
+                lds_barrier();  // every region read back: the buffer takes copies again
+#pragma unroll
+                for (int u = 0; u < GW; ++u)
+#pragma unroll
+                    for (int t = 0; t < kXTiles; ++t) acc[u][t] = f4{0.f, 0.f, 0.f, 0.f};
+                after_out = true;
+            }
+        }
+    } else {
+        int w = 0;
+        for (; w + PERIOD <= nwin; w += PERIOD)
+            static_for<PERIOD>([&](auto kc) { step(w + decltype(kc)::value, kc); });
+        static_for<PERIOD - 1>([&](auto kc) {
+            if (w + decltype(kc)::value < nwin) step(w + decltype(kc)::value, kc);
+        });
+    }
 
-    // ---- the outputs, through LDS: each wave writes its rows x 128 tokens
-    // into a region of its own (rows padded by 32 bytes, so that the 8 rows a
-    // write instruction touches fall on distinct banks), then stores whole
-    // rows, 16 bytes per lane (a full 256- or 512-byte run per row, instead of
-    // 32- or 64-byte pieces from the instruction's own layout)
-    constexpr int ES = SPLIT ? 4 : 2;
-    constexpr int RSTRIDE = kXTok * ES + 32;
-    constexpr int RB = G::rows_wave * RSTRIDE;       // one wave's region
-    static_assert(RB == x16_out_region(SPLIT, G::rows_wave), "one region formula");
+    // ---- the outputs of the last tile (all staging buffers free)
     constexpr int WPA = BUFCAP / RB;                 // regions per staging buffer
     static_assert(WPA >= 1 && WPA * NBUF >= NW, "output regions fit the staging buffers");
-    constexpr bool GELU_OK = x16_gelu_fits(SPLIT, G::rows_wave, NW, BUFCAP, NBUF);
     const bool gelu = GELU_OK && epi == NMG_EPILOGUE_GELU;  // the host asks only when it fits
     // the GELU table's non-rule entries, 16 bytes a thread and step, all loads
     // in flight together before the barrier (the buffers are free after it)
@@ -623,87 +760,7 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
                                        : (lds_char *)xs1 + kGeluNegBytes + (wave - W2 - W3 - W0) * RB;
         }
     }
-#pragma unroll
-    for (int u = 0; u < GW; ++u) {
-        const float sc = SPLIT ? __builtin_ldexpf(1.f, -(int)scale[ug[u]]) : 1.f;
-#pragma unroll
-        for (int t = 0; t < kXTiles; ++t) {
-            f4 d = acc[u][t];
-            const uint32_t col = (uint32_t)((16 * t + 4 * q) * ES);
-            if constexpr (SPLIT) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) d[i] = add_row_ror8(d[i]) * sc;
-                if (p < 8) *(__attribute__((address_space(3))) f4 *)(ob + (u * RU + p) * RSTRIDE + col) = d;
-            } else {
-                if (U16 || p < 8)
-                    *(lds_u2 *)(ob + (u * RU + p) * RSTRIDE + col) =
-                        u32x2{pack_h2((_Float16)d[0], (_Float16)d[1]), pack_h2((_Float16)d[2], (_Float16)d[3])};
-            }
-        }
-    }
-    constexpr int LPR = kXTok * ES / 16;              // lanes per row
-    constexpr int RPI = 64 / LPR;                     // rows per instruction
-    const int orow = lane / LPR, ocol = lane % LPR;
-    const int tok = t0 + ocol * (16 / ES);
-    // a wave whose rows and tokens are all inside Y stores without a guard per
-    // row, so that the compiler may overlap the rows' LDS reads
-    const bool whole = row_w + G::rows_wave <= M && t0 + kXTok <= N;
-    auto store_rows = [&](auto guarded) __attribute__((always_inline)) {
-#pragma unroll
-    for (int r0 = 0; r0 < G::rows_wave; r0 += RPI) {
-        const int r = r0 + orow;
-        f4 v = *(__attribute__((address_space(3))) f4 *)(ob + r * RSTRIDE + ocol * 16);
-        const int row = row_w + r;
-        if (!decltype(guarded)::value || (row < M && tok < N)) {
-            if constexpr (GELU_OK) {
-                if (gelu) {
-                    typedef __attribute__((address_space(3))) const uint16_t lds_u16;
-                    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-                    const u32x4 a = __builtin_bit_cast(u32x4, v);  // 8 binary16, two per word
-                    u32x4 o = {0u, 0u, 0u, 0u};
-                    lds_u16 *const tab0 = (lds_u16 *)(lds_char *)xs0;
-                    lds_u16 *const tab1 = (lds_u16 *)(lds_char *)xs1;
-                    // branch-free: one LDS read per element, at an in-bounds
-                    // entry of the sign's table (all 8 issued before any is
-                    // used), then the rule where the table has no entry
-                    uint32_t bb[8], lim[8], tv[8];
-#pragma unroll
-                    for (int i = 0; i < 8; ++i) {
-                        bb[i] = (a[i >> 1] >> (16 * (i & 1))) & 0xffffu;
-                        lim[i] = (bb[i] >> 15) ? (uint32_t)(NMG_GELU_F16_NEGZERO_FROM - 0x8001)
-                                               : (uint32_t)(NMG_GELU_F16_IDENTITY_FROM - 1);
-                        tv[i] = ((bb[i] >> 15) ? tab1 : tab0)[min(bb[i] & 0x7fffu, lim[i])];
-                    }
-#pragma unroll
-                    for (int i = 0; i < 8; ++i) {
-                        const uint32_t b = bb[i];
-                        const uint32_t rule = b <= 0x7c00u ? b
-                                              : (b - 0x8000u) < 0x7c00u ? 0x8000u
-                                                                       : (uint32_t)NMG_GELU_F16_NAN_OUT;
-                        o[i >> 1] |= ((b & 0x7fffu) <= lim[i] ? tv[i] : rule) << (16 * (i & 1));
-                    }
-                    v = __builtin_bit_cast(f4, o);
-                }
-            }
-            if (R_ != nullptr) {
-                const f4 rv = *reinterpret_cast<const f4 *>(reinterpret_cast<const char *>(R_) +
-                                                            ((int64_t)row * ldr + tok) * ES);
-                if constexpr (SPLIT) {
-                    v = v + rv;
-                } else {
-                    const h8 a = __builtin_bit_cast(h8, v), b = __builtin_bit_cast(h8, rv);
-                    h8 o;
-#pragma unroll
-                    for (int i = 0; i < 8; ++i) o[i] = (_Float16)((float)a[i] + (float)b[i]);
-                    v = __builtin_bit_cast(f4, o);
-                }
-            }
-            store_y(v, reinterpret_cast<f4 *>(reinterpret_cast<char *>(Y_) + ((int64_t)row * ldy + tok) * ES));
-        }
-    }
-    };
-    if (whole) store_rows(std::false_type{});
-    else store_rows(std::true_type{});
+    tile_out(ob, t0 + (ntile - 1) * kXTok, gelu);
 }
 
 }  // namespace
@@ -787,7 +844,7 @@ struct X16Out {
     int64_t ldr;
 };
 
-template <bool SPLIT, int NS, bool U16, int GW, int NW, int NSTG, int DP>
+template <bool SPLIT, int NS, bool U16, int GW, int NW, int NSTG, int DP, int TPW = 1>
 nmg_status launch_x16_k(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
                         int N, const X16Out &o, hipStream_t stream) {
     using G = XGeom<SPLIT, U16, GW, NW>;
@@ -798,11 +855,11 @@ nmg_status launch_x16_k(const nmg_layout *L, const void *prepared, const void *X
     const XPrep P = x16_prep_layout(L, G::rows_unit);
     const char *base = static_cast<const char *>(prepared);
     const int row_blocks = (L->M + G::rows_wg - 1) / G::rows_wg;
-    const int grid = row_blocks * ((N + kXTok - 1) / kXTok);
+    const int grid = row_blocks * (((N + kXTok - 1) / kXTok + TPW - 1) / TPW);
     const h8 *fr = reinterpret_cast<const h8 *>(base + P.frag);
     const uint16_t *of = reinterpret_cast<const uint16_t *>(base + P.offs);
     const int8_t *sc = reinterpret_cast<const int8_t *>(base + P.scale);
-    hipLaunchKernelGGL((k_spmm_x16<SPLIT, NS, U16, GW, NW, NSTG, DP>), dim3(grid), dim3(64 * NW), 0,
+    hipLaunchKernelGGL((k_spmm_x16<SPLIT, NS, U16, GW, NW, NSTG, DP, TPW>), dim3(grid), dim3(64 * NW), 0,
                        stream, fr, of, sc, X, ldx, o.Y, o.ldy,
                        o.epi == NMG_EPILOGUE_ADD ? o.R : nullptr, o.ldr, o.epi, L->M, L->K, N,
                        L->m, P.nwin, row_blocks);
@@ -832,6 +889,25 @@ constexpr int x16_dp_of() {
     return NW == 6 ? 3 : 2;
 }
 
+// Two token tiles per workgroup (binary16 workgroups of 3 units of 8 rows a
+// wave, whose outputs fit one staging buffer; no GELU): when one tile a workgroup would take more than one round of
+// workgroups and two tiles a workgroup take one, and every tile's windows end
+// a block of the pipeline's static rotation (6 steps at two windows ahead).
+// The workgroup's window pipeline then runs on into its second tile while
+// the first tile's outputs drain.
+template <bool SPLIT, bool U16, int GW, int NW>
+constexpr bool x16_two_tile_shape() {
+    return !SPLIT && !U16 && GW == 3 && (NW == 8 || NW == 6);
+}
+inline bool x16_two_tiles(const nmg_layout *L, int64_t N, int rows_wg, int wbytes, int epi) {
+    const int nwin = (L->C * L->n + kXSlots - 1) / kXSlots;
+    const int64_t tt = (N + kXTok - 1) / kXTok;
+    const int64_t rbs = (L->M + rows_wg - 1) / rows_wg;
+    const int64_t cus = device_cus();
+    return epi != NMG_EPILOGUE_GELU && nwin % 6 == 0 && wbytes <= x16_buf_cap<false, 2>() &&
+           rbs * tt > cus && rbs * ((tt + 1) / 2) <= cus;
+}
+
 template <bool SPLIT, int NS, bool U16, int GW, int NW = x16_waves<SPLIT>()>
 nmg_status launch_x16_s(const nmg_layout *L, const void *prepared, const void *X, int64_t ldx,
                         int N, const X16Out &Y, hipStream_t stream) {
@@ -839,9 +915,16 @@ nmg_status launch_x16_s(const nmg_layout *L, const void *prepared, const void *X
     const int r = s <= 2 ? 2 : s <= 4 ? 4 : s <= 6 ? 6 : 8;
     // a window must fit the buffers of the instantiation's depth
     const int wbytes = x16_buffer_bytes(L->n, L->m, SPLIT ? 512 : 256);
+    const bool two = x16_two_tile_shape<SPLIT, U16, GW, NW>() &&
+                     x16_two_tiles(L, N, XGeom<SPLIT, U16, GW, NW>::rows_wg, wbytes, Y.epi);
 #define X16_CASE(V)                                                                                \
     case V:                                                                                        \
         if constexpr (x16_nstg_used<SPLIT, NS, NW>(V)) {                                           \
+            if constexpr (x16_two_tile_shape<SPLIT, U16, GW, NW>()) {                              \
+                if (two)                                                                           \
+                    return launch_x16_k<SPLIT, NS, U16, GW, NW, V, 2, 2>(L, prepared, X, ldx, N,   \
+                                                                         Y, stream);               \
+            }                                                                                      \
             constexpr int DPV = x16_dp_of<SPLIT, NS, NW, V>();                                     \
             if (wbytes <= x16_buf_cap<SPLIT, DPV>())                                               \
                 return launch_x16_k<SPLIT, NS, U16, GW, NW, V, DPV>(L, prepared, X, ldx, N, Y,     \

@@ -283,6 +283,37 @@ def test_x16_random(nmg, M, K, N, n, m, g, dtype, wscale, xscale):
     check_product(Y, Yref, B, dtype, f"x16 {kernel}", L.C * L.n)
 
 
+@pytest.mark.parametrize("M,N", [(3072, 4096), (3072, 3960), (2304, 4096), (2304, 3960)])
+def test_x16_two_tiles(nmg, M, N):
+    """Layers whose one-tile grid takes two rounds of workgroups (FFN up and
+    QKV shapes, 2:8:8 binary16) run two token tiles per workgroup, the second
+    tile's windows staged while the first tile's outputs drain; 3960 tokens
+    leave the last workgroup one ragged tile.  Every output is bit for bit
+    what the one-tile launch gives on column blocks of 1024 tokens (its grid
+    fits one round), also with the residual sum, and sampled outputs meet the
+    bound against the oracle."""
+    K, n, m, g = 768, 2, 8, 8
+    W = synth.normal((M, K), 51 + M, 0.02, torch.float16)
+    X = synth.normal((K, N), 52 + N, 1.0, torch.float16)
+    R = synth.normal((M, N), 53 + N, 1.0, torch.float16).to(DEV)
+    v, idx, L, rv, ridx = check_compress(nmg, W, n, m, g, "two tiles")
+    print(f"[x16 two tiles] {L} N={N}", flush=True)
+    prepared = nmg.x16_prepare(v, idx, L)
+    Xd = X.to(DEV)
+    Y = nmg.spmm_x16_epilogue(L, prepared, Xd)
+    Ya = nmg.spmm_x16_epilogue(L, prepared, Xd, "add", R)
+    Yb = torch.full_like(Y, 7.0)
+    Yab = torch.full_like(Y, 7.0)
+    for c0 in range(0, N, 1024):
+        c1 = min(N, c0 + 1024)
+        nmg.spmm_x16_epilogue(L, prepared, Xd[:, c0:c1], Y=Yb[:, c0:c1])
+        nmg.spmm_x16_epilogue(L, prepared, Xd[:, c0:c1], "add", R[:, c0:c1], Y=Yab[:, c0:c1])
+    torch.cuda.synchronize()
+    assert torch.equal(Y.view(torch.int16), Yb.view(torch.int16))
+    assert torch.equal(Ya.view(torch.int16), Yab.view(torch.int16))
+    check_sampled(nmg, v, idx, L, X, Y, rv, ridx, what="x16 two tiles")
+
+
 def random_large(count=12, seed=2306):
     """Seeded random layouts at the workloads' scale (the launch shapes small
     cases never reach: 4 tokens per lane, several rounds of workgroups,
