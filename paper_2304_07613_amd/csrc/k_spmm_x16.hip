@@ -663,17 +663,25 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
     char *const bufs[4] = {xs0, xs1, xs2, xs3};
     Ops ops[NOPS];
     uint32_t aa[2][GW][2];
-    static_for<DIST>([&](auto dc) { load_ops(decltype(dc)::value, ops[decltype(dc)::value]); });
     if constexpr (SPLIT) {
+        load_ops(0, ops[0]);
         stage_issue(0, xs0);
+        stage_write(xs0);
+        wait_all_memory();
+        addresses(ops[0], aa[0]);
+        __syncthreads();
     } else {
-        static_for<DIST>([&](auto dc) { stage_issue(decltype(dc)::value, bufs[decltype(dc)::value]); });
+        // window by window, operands then copies; window 0 starts once its
+        // own copies have landed (the count at a window's end: the (DIST -
+        // 1) (2 GW + NSTG) loads of windows 1 .. DIST - 1 may stay in
+        // flight); step 0 makes window 1's addresses
+        static_for<DIST>([&](auto dc) {
+            load_ops(decltype(dc)::value, ops[decltype(dc)::value]);
+            stage_issue(decltype(dc)::value, bufs[decltype(dc)::value]);
+        });
+        addresses(ops[0], aa[0]);
+        window_barrier<(DIST - 1) * (2 * GW + NSTG)>();
     }
-    stage_write(xs0);
-    wait_all_memory();
-    addresses(ops[0], aa[0]);
-    if constexpr (DIST >= 2) addresses(ops[1], aa[1]);
-    __syncthreads();
     // step w (W6 = w % PERIOD, so that operand sets, address sets and buffers
     // rotate statically): window w from bufs[W6 % NBUF]
     constexpr int PERIOD = NOPS == 4 ? 4 : 6;  // a multiple of NOPS, NBUF and 2
