@@ -290,8 +290,8 @@ def test_x16_two_tiles(nmg, M, N):
     tile's windows staged while the first tile's outputs drain; 3960 tokens
     leave the last workgroup one ragged tile.  Every output is bit for bit
     what the one-tile launch gives on column blocks of 1024 tokens (its grid
-    fits one round), also with the residual sum, and sampled outputs meet the
-    bound against the oracle."""
+    fits one round), also with the residual sum and on row-strided operands,
+    and sampled outputs meet the bound against the oracle."""
     K, n, m, g = 768, 2, 8, 8
     W = synth.normal((M, K), 51 + M, 0.02, torch.float16)
     X = synth.normal((K, N), 52 + N, 1.0, torch.float16)
@@ -308,9 +308,18 @@ def test_x16_two_tiles(nmg, M, N):
         c1 = min(N, c0 + 1024)
         nmg.spmm_x16_epilogue(L, prepared, Xd[:, c0:c1], Y=Yb[:, c0:c1])
         nmg.spmm_x16_epilogue(L, prepared, Xd[:, c0:c1], "add", R[:, c0:c1], Y=Yab[:, c0:c1])
+    # the two-tile launch on row-strided X, R and Y (views of wider buffers)
+    Xw = torch.zeros((K, N + 64), dtype=torch.float16, device=DEV)
+    Rw = torch.zeros((M, N + 72), dtype=torch.float16, device=DEV)
+    Yw = torch.full((M, N + 40), 7.0, dtype=torch.float16, device=DEV)
+    Xw[:, :N] = Xd
+    Rw[:, 8:N + 8] = R
+    nmg.spmm_x16_epilogue(L, prepared, Xw[:, :N], "add", Rw[:, 8:N + 8], Y=Yw[:, :N])
     torch.cuda.synchronize()
     assert torch.equal(Y.view(torch.int16), Yb.view(torch.int16))
     assert torch.equal(Ya.view(torch.int16), Yab.view(torch.int16))
+    assert torch.equal(Yw[:, :N].view(torch.int16), Ya.view(torch.int16))
+    assert bool((Yw[:, N:] == 7.0).all())
     check_sampled(nmg, v, idx, L, X, Y, rv, ridx, what="x16 two tiles")
 
 
