@@ -243,6 +243,31 @@ __device__ __forceinline__ void lds_copy16(const E *src, E *lds) {
 #endif
 }
 
+// The same copy as a buffer load with an LDS destination (buffer_load_dwordx4
+// ... lds): 16 bytes per lane from byte offset `off` of the buffer `r` into
+// LDS at lds + 16 * lane (`lds` wave-uniform).  The compiler takes a global
+// (flat-encoded) LDS copy in flight as an access to both memory and LDS, and
+// then makes every later use of a loaded register or LDS read wait for all
+// of them (vmcnt(0) / lgkmcnt(0)); buffer copies are counted like other
+// loads, so its waits stay counts.  The descriptor covers `bytes` from
+// `base` (raw: stride 0, 32-bit data format, no swizzle or thread-id offset,
+// the gfx9-family raw-buffer word 3); offsets must fit 32 bits.
+#if defined(__HIP_DEVICE_COMPILE__)
+typedef __amdgpu_buffer_rsrc_t buf_rsrc_t;
+__device__ __forceinline__ buf_rsrc_t buf_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
+                                             0x00020000);
+}
+__device__ __forceinline__ void lds_copy16_buf(buf_rsrc_t r, uint32_t off, void *lds) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void *)lds, 16,
+                                             (int)off, 0, 0, 0);
+}
+#else
+typedef int buf_rsrc_t;
+__device__ inline buf_rsrc_t buf_rsrc(const void *, uint32_t) { return 0; }
+__device__ inline void lds_copy16_buf(buf_rsrc_t, uint32_t, void *) {}
+#endif
+
 // Wait for every outstanding memory operation of this wave.
 __device__ __forceinline__ void wait_all_memory() {
 #if defined(__HIP_DEVICE_COMPILE__)

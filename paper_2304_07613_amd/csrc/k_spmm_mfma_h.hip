@@ -168,12 +168,14 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
     const int lane_x1 = sub_off + min(t0 + (copy_tk ^ 64), N - 8);
     // r / m by a multiply, exact for r < 2^16 / m (rows of a window: r <= 128)
     const uint32_t inv_m = (65536u + (uint32_t)m - 1) / (uint32_t)m;
+    // the copies are buffer loads (lds_copy16_buf; K ldx < 2^31 elements, so
+    // every byte offset fits 32 bits)
+    const buf_rsrc_t xrs = buf_rsrc(X, (uint32_t)((int64_t)K * ldx * 2));
     auto issue_copies = [&](int win, _Float16 *buf) {
         const int ninst = (rpw + RPI - 1) / RPI;
         for (int j = wave; j < ninst; j += nwaves) {
             const int rb = __builtin_amdgcn_readfirstlane(j * RPI);   // first row in the window
             const int kb = __builtin_amdgcn_readfirstlane(win * rpw + rb);   // and in X
-            const _Float16 *xb = X + (int64_t)kb * ldx;
             int lx = lane_x0;
             if constexpr (TPL == 4) {
                 // RPI == 2: the chunk parities of rows rb and rb + 1
@@ -185,7 +187,7 @@ __global__ __launch_bounds__(64 * kHalfMaxWaves) void k_spmm_mfma_h(
             const int lim = K - kb;
             const int clamp = __builtin_amdgcn_readfirstlane((lim - 1) * (int)ldx);
             lx = copy_sub < lim ? lx : lx - sub_off + clamp;
-            lds_copy16(xb + lx, buf + rb * TN);
+            lds_copy16_buf(xrs, ((uint32_t)kb * (uint32_t)ldx + (uint32_t)lx) * 2u, buf + rb * TN);
         }
     };
 

@@ -120,7 +120,9 @@ __global__ __launch_bounds__(DIRECT ? 64 * kFastMaxWaves : 64 * kFastMaxWaves / 
             wv = x;
         }
     };
-    // X rows of a window into LDS
+    // X rows of a window into LDS, by buffer loads (lds_copy16_buf; host: the
+    // byte offsets of X fit 32 bits on this path)
+    const buf_rsrc_t xrs = buf_rsrc(X, DIRECT ? (uint32_t)((int64_t)K * ldx * (int64_t)sizeof(T)) : 0u);
     auto issue_direct = [&](int win, SE *buf) {
         if constexpr (DIRECT) {
             // lane l copies 16 bytes: row l / LPR, elements EPL * (l % LPR) ..
@@ -130,12 +132,11 @@ __global__ __launch_bounds__(DIRECT ? 64 * kFastMaxWaves : 64 * kFastMaxWaves / 
             const int lane_x = sub * (int)ldx + t0 + ce;  // host checked: K * ldx < 2^31
             for (int j = wave; j < ninst; j += nwaves) {
                 const int kb = xr0 + j * RPI;  // first row of this instruction (uniform)
-                if (kb + RPI <= K) {
-                    lds_copy16(X + (int64_t)kb * ldx + lane_x, buf + j * RPI * TN);
-                } else {
-                    const int k = min(kb + sub, K - 1);  // rows past K: never selected
-                    lds_copy16(X + (int64_t)k * ldx + t0 + ce, buf + j * RPI * TN);
-                }
+                // rows past K (the last window): the last row, never selected
+                const uint32_t el = kb + RPI <= K
+                                        ? (uint32_t)kb * (uint32_t)ldx + (uint32_t)lane_x
+                                        : (uint32_t)min(kb + sub, K - 1) * (uint32_t)ldx + (uint32_t)(t0 + ce);
+                lds_copy16_buf(xrs, el * (uint32_t)sizeof(T), buf + j * RPI * TN);
             }
         } else {
             (void)win;
@@ -335,9 +336,11 @@ nmg_status launch_fast_ut(const nmg_layout *L, const void *values, const uint8_t
                           const void *X, int64_t ldx, int N, void *Y, int64_t ldy,
                           hipStream_t stream) {
     const bool xvec = x_vectorisable(L, X, ldx);
-    // direct copies move 16 bytes per lane: 16-byte rows and whole token tiles
+    // direct copies move 16 bytes per lane: 16-byte rows and whole token
+    // tiles; their buffer offsets must fit 32 bits
     const bool direct = aligned(X, 16) && (ldx * (int64_t)sizeof(T)) % 16 == 0 &&
-                        N % (64 * TPL) == 0;
+                        N % (64 * TPL) == 0 &&
+                        (int64_t)L->K * ldx * (int64_t)sizeof(T) <= (int64_t)0xffffffff;
 #define NMG_FAST(KSW)                                                                           \
     return direct ? launch_fast_v<T, U, KSW, TPL, true>(L, values, indices, X, ldx, N, Y, ldy,   \
                                                         xvec, stream)                           \

@@ -84,29 +84,6 @@ __device__ __attribute__((aligned(16))) const uint16_t g_x16_gelu[65536] = {
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) u32x2 lds_u2;
 
-// The copies of X into LDS are buffer loads with an LDS destination
-// (buffer_load_dwordx4 ... lds: 16 bytes per lane to lds + 16 * lane, `lds`
-// wave-uniform), not their global (flat) form: the compiler takes a flat LDS
-// copy in flight as an access to both memory and LDS, and then makes every
-// later use of a loaded register, or LDS read, wait for all memory
-// operations (vmcnt(0)) -- each window would wait for the copies of the
-// windows after it.  Buffer copies are counted like other loads.  The
-// descriptor covers `bytes` from `base` (raw: stride 0, 32-bit data format,
-// no swizzle or thread-id offset -- the gfx9-family raw-buffer word 3).
-#if defined(__HIP_DEVICE_COMPILE__)
-typedef __amdgpu_buffer_rsrc_t x_rsrc_t;
-__device__ __forceinline__ x_rsrc_t x_rsrc(const void *base, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
-}
-__device__ __forceinline__ void lds_copy16_buf(x_rsrc_t r, uint32_t off, lds_char *lds) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void *)lds, 16, (int)off, 0, 0, 0);
-}
-#else
-typedef int x_rsrc_t;
-__device__ inline x_rsrc_t x_rsrc(const void *, uint32_t) { return 0; }
-__device__ inline void lds_copy16_buf(x_rsrc_t, uint32_t, lds_char *) {}
-#endif
-
 // The transposing LDS read of 8 bytes at `p`.
 __device__ __forceinline__ h4 lds_read_tr(lds_char *p) {
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -376,9 +353,10 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
 
     // ---- staging
     const float *Xf = reinterpret_cast<const float *>(X_);
-    // binary16 X as a buffer of K rows (host: K ldx < 2^31 elements, so every
-    // byte offset fits 32 bits)
-    const x_rsrc_t xr16 = x_rsrc(X_, SPLIT ? 0u : (uint32_t)((int64_t)K * ldx * 2));
+    // binary16 X as a buffer of K rows, copied into LDS by buffer loads (see
+    // lds_copy16_buf; host: K ldx < 2^31 elements, so every byte offset fits
+    // 32 bits)
+    const buf_rsrc_t xr16 = buf_rsrc(X_, SPLIT ? 0u : (uint32_t)((int64_t)K * ldx * 2));
     // SPLIT: item i of a window = (row i / 32, tokens 4 (i % 32) .. +3); lane
     // takes items lane_g + k 64 NW (rows st_row0 + k SROWS, one token offset);
     // items past the last are clamped to the last row (a duplicate writes the
@@ -417,7 +395,7 @@ __global__ __launch_bounds__(64 * NW) void k_spmm_x16(
             const int xr = min(k0 + row0 + cp_sub, K - 1);
             const int tok = min(t0 + tj * kXTok + cp_tok, N - 8);
             lds_copy16_buf(xr16, ((uint32_t)xr * (uint32_t)ldx + (uint32_t)tok) * 2u,
-                           (lds_char *)(buf + c * cs + o * ROWB));
+                           buf + c * cs + o * ROWB);
         }
     };
     auto stage_issue = [&](int w, char *buf) __attribute__((always_inline)) {
