@@ -229,27 +229,14 @@ __device__ __forceinline__ int xcd_tile(int i, int total) {
     return x * per + (x < rem ? x : rem) + j;
 }
 
-// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane
-// (global_load_lds_dwordx4; `lds` must be wave-uniform).  The builtin exists
-// only in the device pass.
-template <typename E>
-__device__ __forceinline__ void lds_copy16(const E *src, E *lds) {
-#if defined(__HIP_DEVICE_COMPILE__)
-    __builtin_amdgcn_global_load_lds(reinterpret_cast<const float *>(src),
-                                     reinterpret_cast<float *>(lds), 16, 0, 0);
-#else
-    (void)src;
-    (void)lds;
-#endif
-}
-
-// The same copy as a buffer load with an LDS destination (buffer_load_dwordx4
-// ... lds): 16 bytes per lane from byte offset `off` of the buffer `r` into
-// LDS at lds + 16 * lane (`lds` wave-uniform).  The compiler takes a global
-// (flat-encoded) LDS copy in flight as an access to both memory and LDS, and
-// then makes every later use of a loaded register or LDS read wait for all
-// of them (vmcnt(0) / lgkmcnt(0)); buffer copies are counted like other
-// loads, so its waits stay counts.  The descriptor covers `bytes` from
+// 16 bytes per lane from global memory straight into LDS: a buffer load with
+// an LDS destination (buffer_load_dwordx4 ... lds) from byte offset `off` of
+// the buffer `r` to lds + 16 * lane (`lds` wave-uniform).  Not the global
+// form (global_load_lds_dwordx4): the compiler takes a flat-encoded LDS copy
+// in flight as an access to both memory and LDS, and then makes every later
+// use of a loaded register or LDS read wait for all memory operations
+// (vmcnt(0) / lgkmcnt(0)); buffer copies are counted like other loads, so
+// its waits stay counts.  The descriptor covers `bytes` from
 // `base` (raw: stride 0, 32-bit data format, no swizzle or thread-id offset,
 // the gfx9-family raw-buffer word 3); offsets must fit 32 bits.
 #if defined(__HIP_DEVICE_COMPILE__)

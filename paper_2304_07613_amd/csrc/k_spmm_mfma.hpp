@@ -34,8 +34,9 @@ __device__ __forceinline__ float tok_part(const typename TokVec<TPL>::type &v, i
 // U: rows per group unit (U divides g, U % 4 == 0, U <= 32); KSW: k-slots per
 // window (a power of two <= 16 that n divides; a window is KSW/n whole chunks);
 // TPL: tokens per lane (workgroup token tile = 64 * TPL); DIRECT: X windows go
-// from global memory straight to LDS (global_load_lds_dwordx4), which needs
-// binary32 X, 16-byte aligned rows and whole token tiles; otherwise X passes
+// from global memory straight to LDS (buffer loads with an LDS destination),
+// which needs binary32 X, 16-byte aligned rows, whole token tiles and byte
+// offsets of X within 32 bits; otherwise X passes
 // through registers (and binary16 is widened on the way).
 //
 // Two LDS buffers, one barrier per window: window w is computed from one
@@ -89,7 +90,9 @@ __global__ __launch_bounds__(kBlock, 2) void k_spmm_mfma(
         pair_chunk_row[r] = (s / n) * m;
     }
 
-    // ---- staging of the X rows of a window
+    // ---- staging of the X rows of a window (direct: buffer loads,
+    // lds_copy16_buf; host: the byte offsets of X fit 32 bits)
+    const buf_rsrc_t xrs = buf_rsrc(X, DIRECT ? (uint32_t)((int64_t)K * ldx * 4) : 0u);
     auto issue_direct = [&](int win, float *buf) {
         if constexpr (DIRECT) {
             // one instruction moves RPI rows (1 KB); lane l writes 16 bytes at
@@ -100,7 +103,8 @@ __global__ __launch_bounds__(kBlock, 2) void k_spmm_mfma(
             for (int j = wave; j < ninst; j += 4) {
                 // rows past K are loaded from row K-1: never selected
                 const int k = min(xr0 + j * RPI + sub, K - 1);
-                lds_copy16(X + (int64_t)k * ldx + t0 + 4 * c4, buf + j * RPI * TN);
+                lds_copy16_buf(xrs, ((uint32_t)k * (uint32_t)ldx + (uint32_t)(t0 + 4 * c4)) * 4u,
+                               buf + j * RPI * TN);
             }
         } else {
             (void)win;
@@ -281,8 +285,9 @@ nmg_status launch_mfma_ut(const nmg_layout *L, int ksw, const void *values,
     const bool xvec = x_vectorisable(L, X, ldx);
     const bool yvec = aligned(Y, 2 * elem_size(L->dtype)) && ldy % 2 == 0;
     if constexpr (std::is_same<T, float>::value) {
-        // direct global -> LDS staging: 16-byte rows and whole token tiles
-        if (xvec && N % (64 * TPL) == 0)
+        // direct global -> LDS staging: 16-byte rows, whole token tiles and
+        // byte offsets of X within 32 bits
+        if (xvec && N % (64 * TPL) == 0 && (int64_t)L->K * ldx * 4 <= (int64_t)0xffffffff)
             return launch_mfma_utd<T, U, TPL, true>(L, ksw, values, indices, X, ldx, N, Y, ldy,
                                                     xvec, yvec, stream);
     }

@@ -80,11 +80,14 @@ __global__ __launch_bounds__(64 * kVsWaves) void k_spmm_valu_s(
     // tokens past N: the row's last 16 bytes, never stored)
     const int copy_sub = lane / LPR;
     const int copy_tok = min(t0 + EPL * (lane % LPR), N - EPL);   // host checked: N % EPL == 0
+    // (buffer loads, lds_copy16_buf; host: the byte offsets of X fit 32 bits)
+    const buf_rsrc_t xrs = buf_rsrc(X, (uint32_t)((int64_t)K * ldx * (int64_t)sizeof(T)));
     auto issue_copies = [&](int win, T *buf) {
         const int ninst = (rpw + RPI - 1) / RPI;
         for (int j = wave; j < ninst; j += kVsWaves) {
             const int k = min(win * rpw + j * RPI + copy_sub, K - 1);
-            lds_copy16(X + (int64_t)k * ldx + copy_tok, buf + j * RPI * kVsTok);  // K * ldx < 2^31
+            lds_copy16_buf(xrs, ((uint32_t)k * (uint32_t)ldx + (uint32_t)copy_tok) * (uint32_t)sizeof(T),
+                           buf + j * RPI * kVsTok);
         }
     };
 
@@ -158,15 +161,15 @@ nmg_status launch_valu_s(const SpmmArgs &a) {
 // The staged vector kernel takes binary32 layouts whose chunks fit the
 // staging buffer (m <= 32 rows of 256 tokens) with n <= 16 (a window of at
 // least one chunk keeps 16 k-slots at most), and X that can be copied 16
-// bytes at a time (X and ldx on 16-byte boundaries, N % 4 == 0); offsets
-// within 31 bits.  (Binary16 layouts of g % 4 != 0 go to the sparse matrix
+// bytes at a time (X and ldx on 16-byte boundaries, N % 4 == 0); value
+// offsets within 31 bits, byte offsets of X within 32 bits.  (Binary16 layouts of g % 4 != 0 go to the sparse matrix
 // instruction, or the vector kernel.)
 bool nmg_internal::spmm_valu_staged_supported(const nmg_layout *L, const void *X, int64_t ldx,
                                               int64_t N) {
     return L->dtype == NMG_F32 && L->m <= vs_rows_max<float>() && L->n <= 4 * kVsGroups &&
            (X == nullptr || aligned(X, 16)) && ldx % 4 == 0 && N % 4 == 0 &&
            (int64_t)L->M * L->C * L->n < ((int64_t)1 << 31) &&
-           (int64_t)L->K * ldx < ((int64_t)1 << 31);
+           (int64_t)L->K * ldx * 4 <= (int64_t)0xffffffff;
 }
 
 nmg_status nmg_internal::spmm_valu_staged(const SpmmArgs &a) { return launch_valu_s<float>(a); }
