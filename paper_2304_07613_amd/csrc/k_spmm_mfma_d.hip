@@ -18,7 +18,17 @@
 namespace {
 
 constexpr int kDRowsWave = 16;   // 4 quads
-constexpr int kDMaxWaves = 16;
+
+// The window, tokens per lane and largest workgroup of each group unit.  Two
+// windows of gathered rows are in registers at once: 4 tokens a lane for
+// units of 8 and 16 rows (up to about 220 registers, so at most 8 waves a
+// workgroup; against 2 tokens and 8-slot windows in 16-wave workgroups,
+// workload 3 40.7 -> 33.1 us, 1:20:8 32.4 -> 23.7, 1:10:8 53.3 -> 38.6),
+// 1 token for units of 4 (whose windows gather 4 rows a slot).
+template <int U> struct DConf;
+template <> struct DConf<16> { static constexpr int ksw = 4, tpl = 4, waves = 8; };
+template <> struct DConf<8> { static constexpr int ksw = 4, tpl = 4, waves = 8; };
+template <> struct DConf<4> { static constexpr int ksw = 4, tpl = 1, waves = 16; };
 
 template <int TPL> struct DTok { typedef float type __attribute__((ext_vector_type(TPL))); };
 template <> struct DTok<1> { typedef float type; };
@@ -28,7 +38,7 @@ __device__ __forceinline__ float d_part(const typename DTok<TPL>::type &v, int p
 }
 
 template <int U, int KSW, int TPL, bool VEC>
-__global__ __launch_bounds__(64 * kDMaxWaves) void k_spmm_mfma_d(
+__global__ __launch_bounds__(64 * DConf<U>::waves) void k_spmm_mfma_d(
     const float *__restrict__ values, const uint8_t *__restrict__ indices,
     const float *__restrict__ X, int64_t ldx, float *__restrict__ Y, int64_t ldy, int M, int K,
     int N, int log2n, int m, int g, int C, int row_tiles, int tiles, int split, bool yvec) {
@@ -270,18 +280,15 @@ __global__ __launch_bounds__(64 * kDMaxWaves) void k_spmm_mfma_d(
     }
 }
 
-// The window and tokens per lane of each group unit: two windows of gathered
-// rows take 32 registers.
-template <int U> struct DConf;
-template <> struct DConf<16> { static constexpr int ksw = 8, tpl = 2; };
-template <> struct DConf<8> { static constexpr int ksw = 4, tpl = 2; };
-template <> struct DConf<4> { static constexpr int ksw = 4, tpl = 1; };
-
 // Row-waves x k-splits per workgroup.  Each shape is priced as rounds of the
-// GPU (waves resident at once, from the runtime's occupancy and the LDS of
-// the reduction) times the windows one wave runs, plus one window's worth
-// per extra split for the reduction; the cheapest wins, and on a tie the one
-// with fewer splits, then more row-waves.
+// GPU times the windows one wave runs, plus one window's worth per extra
+// split for the reduction; the cheapest wins, and on a tie the one with fewer
+// splits, then more row-waves.  A round is as many workgroups per CU as are
+// resident at once (the runtime's occupancy and the LDS of the reduction);
+// a last, partial round counts for the share of it that each CU runs, since
+// the CUs' load paths, not the waves, bound the gathers (1:20:16 on 384
+// workgroups of 16 waves, one and a half rounds: 32.8 us; on 768 of 8, two
+// resident a CU: 24.9).
 struct DShape {
     int nrw, split;
     size_t lds;
@@ -297,8 +304,8 @@ DShape d_shape(const nmg_layout *L, int N) {
     constexpr size_t kWaveLds = (size_t)4 * TPL * 64 * sizeof(v4f);  // one wave's partial sums
     DShape best{1, 1, 0};
     double best_cost = 0.0;
-    for (int split = 1; split <= kDMaxWaves && split <= nwin; split *= 2) {
-        for (int nrw = 1; nrw * split <= kDMaxWaves && nrw <= rws; ++nrw) {
+    for (int split = 1; split <= DConf<U>::waves && split <= nwin; split *= 2) {
+        for (int nrw = 1; nrw * split <= DConf<U>::waves && nrw <= rws; ++nrw) {
             const int wg = nrw * split;
             const size_t lds = split > 1 ? (size_t)wg * kWaveLds : 0;
             if (lds > 65536) continue;
@@ -306,8 +313,8 @@ DShape d_shape(const nmg_layout *L, int N) {
             if (lds > 0) per_cu = std::min<int>(per_cu, (int)(163840 / lds));
             per_cu = std::max(per_cu, 1);
             const int64_t tiles = (int64_t)((rws + nrw - 1) / nrw) * tt;
-            const int64_t rounds = (tiles + (int64_t)cus * per_cu - 1) / ((int64_t)cus * per_cu);
-            const double cost = (double)rounds * ((nwin + split - 1) / split + (split > 1 ? 1 : 0));
+            const double rounds = std::max((double)((tiles + cus - 1) / cus) / per_cu, 1.0);
+            const double cost = rounds * ((nwin + split - 1) / split + (split > 1 ? 1 : 0));
             if (best_cost == 0.0 || cost < best_cost - 1e-9 ||
                 (cost < best_cost + 1e-9 && split == best.split && nrw > best.nrw)) {
                 best = DShape{nrw, split, lds};
@@ -360,14 +367,16 @@ nmg_status nmg_internal::spmm_direct(const SpmmArgs &a) {
 
 // AUTO's choice between this kernel and the staged one.  A staged workgroup of
 // about 8 waves (128 rows) reads all K rows of its token tile; a gathering
-// unit of U rows reads its C * n selected rows.  Gathering wins when that
-// reads fewer bytes, and whenever the staged kernel would leave most CUs idle
-// (it has no k-split).
+// unit of U rows reads its C * n selected rows.  Gathering wins up to 1.75
+// times the staged kernel's rows (measured on 3072 x 768 x 4096: 1:10:8, 1.6
+// times, 38.6 against 53.5 us; 1:20:4, 1.6 times, even; 1:4:16, 2 times, 64.2
+// against 54.6), and whenever the staged kernel would leave most CUs idle (it
+// has no k-split).
 bool nmg_internal::spmm_direct_preferred(const nmg_layout *L, int64_t N, int64_t ldx) {
     if (!spmm_direct_supported(L, ldx)) return false;
     const int64_t U = std::min(mfma_unit(L), 16);
     const int64_t ldv = (int64_t)L->C * L->n;
-    if (128 * ldv <= U * L->K) return true;
+    if (4 * 128 * ldv <= 7 * U * L->K) return true;
     const int64_t staged_waves = (int64_t)((L->M + 15) / 16) * ((N + 127) / 128);
     return staged_waves < 2 * device_cus();
 }
