@@ -367,16 +367,17 @@ nmg_status nmg_internal::spmm_direct(const SpmmArgs &a) {
 
 // AUTO's choice between this kernel and the staged one.  A staged workgroup of
 // about 8 waves (128 rows) reads all K rows of its token tile; a gathering
-// unit of U rows reads its C * n selected rows.  Gathering wins up to 1.75
-// times the staged kernel's rows (measured on 3072 x 768 x 4096: 1:10:8, 1.6
-// times, 38.6 against 53.5 us; 1:20:4, 1.6 times, even; 1:4:16, 2 times, 64.2
-// against 54.6), and whenever the staged kernel would leave most CUs idle (it
-// has no k-split).
+// unit of U rows reads its C * n selected rows.  Units of 8 or more rows (4
+// tokens a lane) win up to 1.75 times the staged kernel's rows (measured on
+// 3072 x 768 x 4096: 1:10:8, 1.6 times, 38.6 against 53.5 us; 1:4:16, 2 times,
+// 64.2 against 54.6), units of 4 (1 token a lane) up to the same rows (1:20:4,
+// 1.6 times, 53.4 against 51.2); gathering also wins whenever the staged
+// kernel would leave most CUs idle (it has no k-split).
 bool nmg_internal::spmm_direct_preferred(const nmg_layout *L, int64_t N, int64_t ldx) {
     if (!spmm_direct_supported(L, ldx)) return false;
     const int64_t U = std::min(mfma_unit(L), 16);
     const int64_t ldv = (int64_t)L->C * L->n;
-    if (4 * 128 * ldv <= 7 * U * L->K) return true;
+    if (4 * 128 * ldv <= (U >= 8 ? 7 : 4) * U * L->K) return true;
     const int64_t staged_waves = (int64_t)((L->M + 15) / 16) * ((N + 127) / 128);
     return staged_waves < 2 * device_cus();
 }
