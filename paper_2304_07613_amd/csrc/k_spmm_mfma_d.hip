@@ -19,16 +19,24 @@ namespace {
 
 constexpr int kDRowsWave = 16;   // 4 quads
 
-// The window, tokens per lane and largest workgroup of each group unit.  Two
-// windows of gathered rows are in registers at once: 4 tokens a lane for
-// units of 8 and 16 rows (up to about 220 registers, so at most 8 waves a
-// workgroup; against 2 tokens and 8-slot windows in 16-wave workgroups,
-// workload 3 40.7 -> 33.1 us, 1:20:8 32.4 -> 23.7, 1:10:8 53.3 -> 38.6),
-// 1 token for units of 4 (whose windows gather 4 rows a slot).
-template <int U> struct DConf;
-template <> struct DConf<16> { static constexpr int ksw = 4, tpl = 4, waves = 8; };
-template <> struct DConf<8> { static constexpr int ksw = 4, tpl = 4, waves = 8; };
-template <> struct DConf<4> { static constexpr int ksw = 4, tpl = 1, waves = 16; };
+// The window, tokens per lane and largest workgroup of each group unit, in two
+// shapes.  Two windows of gathered rows are in registers at once.
+//   WIDE, for layers whose 256-token tiles alone cover the CUs: 4 tokens a
+//   lane and 4-slot windows in workgroups of at most 8 waves (up to about 250
+//   registers; units of 4 rows spill 4, which costs less than one wave a
+//   SIMD: 1:20:4 29.5 us against 34.8 in 4-wave workgroups).  Against the
+//   narrow shape on 3072 x 768 x 4096: 1:20:4 51.6 -> 29.8 us, 1:10:4 90.9 ->
+//   51.6, 1:20:8 32.4 -> 23.7, 1:10:8 53.3 -> 38.6, and on 768 x 3072 x 4096
+//   at 1:10:16 40.7 -> 33.1.
+//   Narrow, for layers that need the k-split to fill the GPU (768 x 768 x 128
+//   at 2:4:4 takes 13.4 us so, 21.2 wide): 16-wave workgroups, 2 tokens a
+//   lane (1 for units of 4).
+__host__ __device__ constexpr int d_waves(int tpl) { return tpl == 4 ? 8 : 16; }
+template <int U, bool WIDE> struct DConf;
+template <int U> struct DConf<U, true> { static constexpr int ksw = 4, tpl = 4, waves = d_waves(4); };
+template <> struct DConf<16, false> { static constexpr int ksw = 8, tpl = 2, waves = d_waves(2); };
+template <> struct DConf<8, false> { static constexpr int ksw = 4, tpl = 2, waves = d_waves(2); };
+template <> struct DConf<4, false> { static constexpr int ksw = 4, tpl = 1, waves = d_waves(1); };
 
 template <int TPL> struct DTok { typedef float type __attribute__((ext_vector_type(TPL))); };
 template <> struct DTok<1> { typedef float type; };
@@ -38,7 +46,7 @@ __device__ __forceinline__ float d_part(const typename DTok<TPL>::type &v, int p
 }
 
 template <int U, int KSW, int TPL, bool VEC>
-__global__ __launch_bounds__(64 * DConf<U>::waves) void k_spmm_mfma_d(
+__global__ __launch_bounds__(64 * d_waves(TPL)) void k_spmm_mfma_d(
     const float *__restrict__ values, const uint8_t *__restrict__ indices,
     const float *__restrict__ X, int64_t ldx, float *__restrict__ Y, int64_t ldy, int M, int K,
     int N, int log2n, int m, int g, int C, int row_tiles, int tiles, int split, bool yvec) {
@@ -293,9 +301,9 @@ struct DShape {
     int nrw, split;
     size_t lds;
 };
-template <int U>
+template <int U, bool WIDE>
 DShape d_shape(const nmg_layout *L, int N) {
-    constexpr int KSW = DConf<U>::ksw, TPL = DConf<U>::tpl;
+    constexpr int KSW = DConf<U, WIDE>::ksw, TPL = DConf<U, WIDE>::tpl, WAVES = DConf<U, WIDE>::waves;
     const void *kern = reinterpret_cast<const void *>(&k_spmm_mfma_d<U, KSW, TPL, true>);
     const int cus = device_cus();
     const int rws = (L->M + kDRowsWave - 1) / kDRowsWave;
@@ -304,8 +312,8 @@ DShape d_shape(const nmg_layout *L, int N) {
     constexpr size_t kWaveLds = (size_t)4 * TPL * 64 * sizeof(v4f);  // one wave's partial sums
     DShape best{1, 1, 0};
     double best_cost = 0.0;
-    for (int split = 1; split <= DConf<U>::waves && split <= nwin; split *= 2) {
-        for (int nrw = 1; nrw * split <= DConf<U>::waves && nrw <= rws; ++nrw) {
+    for (int split = 1; split <= WAVES && split <= nwin; split *= 2) {
+        for (int nrw = 1; nrw * split <= WAVES && nrw <= rws; ++nrw) {
             const int wg = nrw * split;
             const size_t lds = split > 1 ? (size_t)wg * kWaveLds : 0;
             if (lds > 65536) continue;
@@ -325,11 +333,11 @@ DShape d_shape(const nmg_layout *L, int N) {
     return best;
 }
 
-template <int U>
+template <int U, bool WIDE>
 nmg_status launch_d(const SpmmArgs &a) {
-    constexpr int KSW = DConf<U>::ksw, TPL = DConf<U>::tpl;
+    constexpr int KSW = DConf<U, WIDE>::ksw, TPL = DConf<U, WIDE>::tpl;
     const nmg_layout *L = a.L;
-    const DShape sh = d_shape<U>(L, a.N);
+    const DShape sh = d_shape<U, WIDE>(L, a.N);
     const int rws = (L->M + kDRowsWave - 1) / kDRowsWave;
     const int row_tiles = (rws + sh.nrw - 1) / sh.nrw;
     const int tiles = row_tiles * ((a.N + 64 * TPL - 1) / (64 * TPL));
@@ -357,27 +365,33 @@ bool nmg_internal::spmm_direct_supported(const nmg_layout *L, int64_t ldx) {
 }
 
 nmg_status nmg_internal::spmm_direct(const SpmmArgs &a) {
+    // the wide shape when its 256-token tiles of 16 rows cover the CUs
+    const int64_t rws = (a.L->M + kDRowsWave - 1) / kDRowsWave;
+    const bool wide = rws * ((a.N + 255) / 256) >= device_cus();
     switch (std::min(mfma_unit(a.L), 16)) {
-        case 16: return launch_d<16>(a);
-        case 8: return launch_d<8>(a);
-        case 4: return launch_d<4>(a);
+        case 16: return wide ? launch_d<16, true>(a) : launch_d<16, false>(a);
+        case 8: return wide ? launch_d<8, true>(a) : launch_d<8, false>(a);
+        case 4: return wide ? launch_d<4, true>(a) : launch_d<4, false>(a);
         default: return NMG_ERR_UNSUPPORTED;
     }
 }
 
 // AUTO's choice between this kernel and the staged one.  A staged workgroup of
 // about 8 waves (128 rows) reads all K rows of its token tile; a gathering
-// unit of U rows reads its C * n selected rows.  Units of 8 or more rows (4
-// tokens a lane) win up to 1.75 times the staged kernel's rows (measured on
+// unit of U rows reads its C * n selected rows.  In the wide shape, units of
+// 8 or more rows win up to 1.75 times the staged kernel's rows (measured on
 // 3072 x 768 x 4096: 1:10:8, 1.6 times, 38.6 against 53.5 us; 1:4:16, 2 times,
-// 64.2 against 54.6), units of 4 (1 token a lane) up to the same rows (1:20:4,
-// 1.6 times, 53.4 against 51.2); gathering also wins whenever the staged
-// kernel would leave most CUs idle (it has no k-split).
+// 64.2 against 54.6), units of 4 up to 3.5 times (1:10:4, 3.2 times, 51.6
+// against 58.2; 1:4:4, 8 times, 116 against 65); in the narrow one up to the
+// same rows.  Gathering also wins whenever the staged kernel would leave most
+// CUs idle (it has no k-split).
 bool nmg_internal::spmm_direct_preferred(const nmg_layout *L, int64_t N, int64_t ldx) {
     if (!spmm_direct_supported(L, ldx)) return false;
     const int64_t U = std::min(mfma_unit(L), 16);
     const int64_t ldv = (int64_t)L->C * L->n;
-    if (4 * 128 * ldv <= (U >= 8 ? 7 : 4) * U * L->K) return true;
+    const bool wide = (int64_t)((L->M + kDRowsWave - 1) / kDRowsWave) * ((N + 255) / 256) >= device_cus();
+    const int64_t lim = !wide ? 4 : U >= 8 ? 7 : 14;   // 4 x the ratio of rows read
+    if (4 * 128 * ldv <= lim * U * L->K) return true;
     const int64_t staged_waves = (int64_t)((L->M + 15) / 16) * ((N + 127) / 128);
     return staged_waves < 2 * device_cus();
 }

@@ -104,15 +104,15 @@ def test_calls_reject_bad_arguments_before_launch(lib):
     # staging whole windows
     assert lib.nmg_layout_init(ctypes.byref(L), 768, 3072, 1, 10, 16, nmg.F32) == nmg.OK
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_direct"]
-    # units of 8 or 16 rows gather up to 1.75 times the staged kernel's rows:
-    # 1:10:8 (1.6 times) gathers, 1:4:16 (2 times) stages; units of 4 rows up
-    # to the same rows: 1:20:4 (1.6 times) stages
-    assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 1, 10, 8, nmg.F32) == nmg.OK
-    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_direct"]
-    assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 1, 4, 16, nmg.F32) == nmg.OK
-    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_scalar"]
-    assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 1, 20, 4, nmg.F32) == nmg.OK
-    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["mfma_scalar"]
+    # with 256-token tiles that cover the CUs, units of 8 or 16 rows gather up
+    # to 1.75 times the staged kernel's rows: 1:10:8 (1.6 times) gathers,
+    # 1:4:16 (2 times) stages; units of 4 rows up to 3.5 times: 1:10:4 (3.2
+    # times) gathers, 2:8:4 (8 times) stages
+    for (n_, m_, g_), fam in (((1, 10, 8), "mfma_direct"), ((1, 4, 16), "mfma_scalar"),
+                              ((1, 20, 4), "mfma_direct"), ((1, 10, 4), "mfma_direct"),
+                              ((2, 8, 4), "mfma_scalar")):
+        assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, n_, m_, g_, nmg.F32) == nmg.OK
+        assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS[fam], (n_, m_, g_)
     # a layer too small to fill the GPU without splitting its k-slots
     assert lib.nmg_layout_init(ctypes.byref(L), 768, 768, 2, 4, 4, nmg.F32) == nmg.OK
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 128) == nmg.KERNELS["mfma_direct"]

@@ -371,6 +371,27 @@ def test_random_large(nmg, M, K, N, n, m, g, dtype):
                       f"large {kernel}", L.C * L.n)
 
 
+@pytest.mark.parametrize("M,K,N,n,m,g,xoff", [
+    (3072, 768, 1030, 1, 10, 4, 0), (3056, 768, 1030, 1, 20, 8, 0),
+    (768, 3072, 2046, 1, 10, 16, 0), (3072, 768, 1024, 1, 20, 4, 1),
+    (768, 768, 130, 2, 4, 4, 0), (768, 768, 127, 1, 10, 16, 0), (1536, 768, 200, 1, 20, 8, 1)])
+def test_gather_shapes(nmg, M, K, N, n, m, g, xoff):
+    """The gathering kernel in both its shapes (4 tokens a lane when the
+    256-token tiles cover the CUs, else the k-split one): ragged token tiles,
+    N % 4 != 0 and X rows off 16-byte alignment (element loads), a partial
+    row tile, against the oracle on sampled outputs."""
+    W = synth.normal((M, K), 51 + M + K, 0.02, torch.float32)
+    X = synth.normal((K, N), 52 + N, 1.0, torch.float32)
+    v, idx, L, rv, ridx = check_compress(nmg, W, n, m, g, "gather")
+    Xb = torch.zeros((K, N + 4), dtype=torch.float32, device=DEV)
+    Xd = Xb[:, xoff:xoff + N]
+    Xd.copy_(X.to(DEV))
+    print(f"[spmm] gather {L} N={N} xoff={xoff}", flush=True)
+    Y = nmg.spmm(v, idx, Xd, L, "mfma_direct")
+    torch.cuda.synchronize()
+    check_sampled(nmg, v, idx, L, X, Y, rv, ridx, count=8192, seed=M + N, what="gather")
+
+
 # ------------------------------------------------------ fixed-mask repack
 
 def random_patterns(rng, groups, K, n, m):
