@@ -12,7 +12,8 @@
 // w.
 // The k-slots can also be split over the waves of a workgroup, whose partial
 // sums are added through LDS in split order at the end: a layer with few rows
-// or few tokens (768 x 768 x 128) still gives every CU waves to run.
+// or few tokens (768 x 768 x 128) still gives every CU waves to run.  Layers
+// that fill the GPU anyway take 4 tokens per lane (the wide shape, DConf).
 #include "common.hpp"
 
 namespace {
