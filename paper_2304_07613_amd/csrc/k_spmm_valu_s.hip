@@ -4,8 +4,8 @@
 // and the matrix-core kernels decline.
 //
 // The vector kernel (k_spmm_valu) gathers each row's X rows from global
-// memory, one load per 4 multiply-adds.  Here a workgroup of 64 rows x 256
-// tokens copies a window of whole chunks of X (global -> LDS, 16 bytes per
+// memory, one load per 4 multiply-adds.  Here a workgroup of 64 (or 256) rows
+// x 256 tokens copies a window of whole chunks of X (global -> LDS, 16 bytes per
 // lane) once, and every row reads the rows it selects from LDS: one 16-byte
 // LDS read per lane feeds 4 FMAs, and each staged row serves every row of the
 // workgroup that selects it.  Weights and index bytes of 16 rows x 4 slots
@@ -16,13 +16,18 @@
 namespace {
 
 constexpr int kVsRowsWave = 16;
-constexpr int kVsWaves = 4;
-constexpr int kVsRowsWg = kVsRowsWave * kVsWaves;   // 64 rows
 constexpr int kVsTok = 256;                         // 4 tokens per lane
-constexpr int kVsStageBytes = 32768;                // per staging buffer
 constexpr int kVsGroups = 4;                        // groups of 4 k-slots per window, max
+// Two shapes: workgroups of 4 waves (64 rows) with 32 KB staging buffers, and,
+// where such a window holds a single k-slot (m > 16 at n = 1), 16 waves (256
+// rows, each staged row serving 4 times as many) with 64 KB buffers, so that a
+// window holds several chunks: on 3072 x 768 x 4096 at 1:20:1 220 -> 97 us
+// (the gathering vector kernel: 139); at m <= 10 the small shape is faster
+// (1:10:1 156 against 171 us).
+constexpr int kVsSmallWaves = 4, kVsSmallStage = 32768;
+constexpr int kVsWideWaves = 16, kVsWideStage = 65536;
 
-template <typename T> constexpr int vs_rows_max() { return kVsStageBytes / (kVsTok * (int)sizeof(T)); }
+template <typename T, int SB> constexpr int vs_rows_max() { return SB / (kVsTok * (int)sizeof(T)); }
 
 // 4 staged tokens of row `row` at this lane
 template <typename T>
@@ -31,8 +36,8 @@ __device__ __forceinline__ v4f vs_read(const T *buf, uint32_t row, int lane) {
     return *reinterpret_cast<const v4f *>(buf + row * kVsTok + 4 * lane);
 }
 
-template <typename T>
-__global__ __launch_bounds__(64 * kVsWaves) void k_spmm_valu_s(
+template <typename T, int WAVES, int SB>
+__global__ __launch_bounds__(64 * WAVES) void k_spmm_valu_s(
     const T *__restrict__ values, const uint8_t *__restrict__ indices,
     const T *__restrict__ X, int64_t ldx, T *__restrict__ Y, int64_t ldy, int M, int K, int N,
     int n, int m, int g, int C, int cpw, int row_tiles, int tiles) {
@@ -40,14 +45,14 @@ __global__ __launch_bounds__(64 * kVsWaves) void k_spmm_valu_s(
     constexpr int EPL = 16 / ES;                 // elements per 16-byte copy
     constexpr int LPR = kVsTok / EPL;            // copy lanes per staged row
     constexpr int RPI = 64 / LPR;                // staged rows per copy instruction
-    __shared__ T xs0[kVsStageBytes / ES];
-    __shared__ T xs1[kVsStageBytes / ES];
+    __shared__ T xs0[SB / ES];
+    __shared__ T xs1[SB / ES];
 
     const int tile = xcd_tile(blockIdx.x, tiles);
     const int rt = tile % row_tiles, tt = tile / row_tiles;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int r0 = rt * kVsRowsWg + wave * kVsRowsWave;
+    const int r0 = rt * (kVsRowsWave * WAVES) + wave * kVsRowsWave;
     const int t0 = tt * kVsTok;
     const int ldv = C * n;                       // host checked: M * ldv < 2^31
     const int rpw = cpw * m;                     // staged rows per window (<= vs_rows_max)
@@ -84,7 +89,7 @@ __global__ __launch_bounds__(64 * kVsWaves) void k_spmm_valu_s(
     const buf_rsrc_t xrs = buf_rsrc(X, (uint32_t)((int64_t)K * ldx * (int64_t)sizeof(T)));
     auto issue_copies = [&](int win, T *buf) {
         const int ninst = (rpw + RPI - 1) / RPI;
-        for (int j = wave; j < ninst; j += kVsWaves) {
+        for (int j = wave; j < ninst; j += WAVES) {
             const int k = min(win * rpw + j * RPI + copy_sub, K - 1);
             lds_copy16_buf(xrs, ((uint32_t)k * (uint32_t)ldx + (uint32_t)copy_tok) * (uint32_t)sizeof(T),
                            buf + j * RPI * kVsTok);
@@ -144,16 +149,31 @@ __global__ __launch_bounds__(64 * kVsWaves) void k_spmm_valu_s(
     }
 }
 
+// chunks per window of a staging buffer of SB bytes
+template <typename T, int SB>
+int vs_cpw(const nmg_layout *L) {
+    return std::max(1, std::min(vs_rows_max<T, SB>() / L->m, 4 * kVsGroups / L->n));
+}
+// the wide shape where a small window would hold a single k-slot
 template <typename T>
-nmg_status launch_valu_s(const SpmmArgs &a) {
+bool vs_wide(const nmg_layout *L) { return vs_cpw<T, kVsSmallStage>(L) * L->n < 2; }
+
+template <typename T, int WAVES, int SB>
+nmg_status launch_valu_s_shape(const SpmmArgs &a) {
     const nmg_layout *L = a.L;
-    const int cpw = std::max(1, std::min(vs_rows_max<T>() / L->m, 4 * kVsGroups / L->n));
-    const int row_tiles = (L->M + kVsRowsWg - 1) / kVsRowsWg;
+    const int cpw = vs_cpw<T, SB>(L);
+    const int row_tiles = (L->M + kVsRowsWave * WAVES - 1) / (kVsRowsWave * WAVES);
     const int tiles = row_tiles * ((a.N + kVsTok - 1) / kVsTok);
-    hipLaunchKernelGGL((k_spmm_valu_s<T>), dim3(tiles), dim3(64 * kVsWaves), 0, a.stream,
+    hipLaunchKernelGGL((k_spmm_valu_s<T, WAVES, SB>), dim3(tiles), dim3(64 * WAVES), 0, a.stream,
                        (const T *)a.values, a.indices, (const T *)a.X, a.ldx, (T *)a.Y, a.ldy,
                        L->M, L->K, a.N, L->n, L->m, L->g, L->C, cpw, row_tiles, tiles);
     return launched();
+}
+
+template <typename T>
+nmg_status launch_valu_s(const SpmmArgs &a) {
+    return vs_wide<T>(a.L) ? launch_valu_s_shape<T, kVsWideWaves, kVsWideStage>(a)
+                           : launch_valu_s_shape<T, kVsSmallWaves, kVsSmallStage>(a);
 }
 
 }  // namespace
@@ -166,7 +186,7 @@ nmg_status launch_valu_s(const SpmmArgs &a) {
 // instruction, or the vector kernel.)
 bool nmg_internal::spmm_valu_staged_supported(const nmg_layout *L, const void *X, int64_t ldx,
                                               int64_t N) {
-    return L->dtype == NMG_F32 && L->m <= vs_rows_max<float>() && L->n <= 4 * kVsGroups &&
+    return L->dtype == NMG_F32 && L->m <= vs_rows_max<float, kVsSmallStage>() && L->n <= 4 * kVsGroups &&
            (X == nullptr || aligned(X, 16)) && ldx % 4 == 0 && N % 4 == 0 &&
            (int64_t)L->M * L->C * L->n < ((int64_t)1 << 31) &&
            (int64_t)L->K * ldx * 4 <= (int64_t)0xffffffff;
@@ -175,10 +195,11 @@ bool nmg_internal::spmm_valu_staged_supported(const nmg_layout *L, const void *X
 nmg_status nmg_internal::spmm_valu_staged(const SpmmArgs &a) { return launch_valu_s<float>(a); }
 
 // AUTO's choice between this kernel and the gathering vector kernel: staging
-// pays when a window holds at least 2 k-slots (with one, as at 1:20, every
-// slot costs a copy and a barrier for a single FMA per row and token).
+// pays when a window holds at least 2 k-slots (with one, every slot costs a
+// copy and a barrier for a single FMA per row and token); the wide shape's
+// windows hold 2 or more chunks for every supported m.
 bool nmg_internal::spmm_valu_staged_preferred(const nmg_layout *L, const void *X, int64_t ldx,
                                               int64_t N) {
     return spmm_valu_staged_supported(L, X, ldx, N) &&
-           std::min(vs_rows_max<float>() / L->m, 4 * kVsGroups / L->n) * L->n >= 2;
+           (vs_wide<float>(L) ? vs_cpw<float, kVsWideStage>(L) : vs_cpw<float, kVsSmallStage>(L)) * L->n >= 2;
 }

@@ -93,9 +93,10 @@ def test_calls_reject_bad_arguments_before_launch(lib):
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 32) == nmg.KERNELS["valu"]    # m > 32
     assert lib.nmg_spmm_with(ctypes.byref(L), nmg.KERNELS["valu_staged"], p, p, p, 32, 32, p, 32,
                              s) == nmg.ERR_UNSUPPORTED
-    # 1:20, g = 1: a window of one k-slot, the gathering vector kernel is faster
+    # 1:20, g = 1: a 32 KB window holds one chunk, so the staged kernel takes
+    # its wide shape (64 KB windows of 3 chunks), faster than gathering
     assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 1, 20, 1, nmg.F32) == nmg.OK
-    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["valu"]
+    assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["valu_staged"]
     assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 1, 10, 1, nmg.F32) == nmg.OK
     assert lib.nmg_spmm_auto_kernel(ctypes.byref(L), 4096) == nmg.KERNELS["valu_staged"]
     assert lib.nmg_layout_init(ctypes.byref(L), 3072, 768, 1, 4, 8, nmg.F32) == nmg.OK
