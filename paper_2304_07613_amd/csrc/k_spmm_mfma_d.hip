@@ -355,6 +355,12 @@ nmg_status launch_d(const SpmmArgs &a) {
     return launched();
 }
 
+// The wide shape when its 256-token tiles of 16 rows cover the CUs.
+bool d_wide(const nmg_layout *L, int64_t N) {
+    const int64_t rws = (L->M + kDRowsWave - 1) / kDRowsWave;
+    return rws * ((N + 255) / 256) >= device_cus();
+}
+
 }  // namespace
 
 // The gathering kernel takes binary32 layouts with g % 4 == 0 and n a power of
@@ -366,9 +372,7 @@ bool nmg_internal::spmm_direct_supported(const nmg_layout *L, int64_t ldx) {
 }
 
 nmg_status nmg_internal::spmm_direct(const SpmmArgs &a) {
-    // the wide shape when its 256-token tiles of 16 rows cover the CUs
-    const int64_t rws = (a.L->M + kDRowsWave - 1) / kDRowsWave;
-    const bool wide = rws * ((a.N + 255) / 256) >= device_cus();
+    const bool wide = d_wide(a.L, a.N);
     switch (std::min(mfma_unit(a.L), 16)) {
         case 16: return wide ? launch_d<16, true>(a) : launch_d<16, false>(a);
         case 8: return wide ? launch_d<8, true>(a) : launch_d<8, false>(a);
@@ -390,8 +394,7 @@ bool nmg_internal::spmm_direct_preferred(const nmg_layout *L, int64_t N, int64_t
     if (!spmm_direct_supported(L, ldx)) return false;
     const int64_t U = std::min(mfma_unit(L), 16);
     const int64_t ldv = (int64_t)L->C * L->n;
-    const bool wide = (int64_t)((L->M + kDRowsWave - 1) / kDRowsWave) * ((N + 255) / 256) >= device_cus();
-    const int64_t lim = !wide ? 4 : U >= 8 ? 7 : 14;   // 4 x the ratio of rows read
+    const int64_t lim = !d_wide(L, N) ? 4 : U >= 8 ? 7 : 14;   // 4 x the ratio of rows read
     if (4 * 128 * ldv <= lim * U * L->K) return true;
     const int64_t staged_waves = (int64_t)((L->M + 15) / 16) * ((N + 127) / 128);
     return staged_waves < 2 * device_cus();
